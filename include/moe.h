@@ -1,0 +1,218 @@
+/*
+ * moe.h -- C ABI of the MI355X (gfx950) routed MoE FFN forward, the hot path
+ * of EPS-MoE (arXiv 2410.12247): top-k softmax gating, expert-sorted
+ * dispatch, the SwiGLU expert FFN run as one grouped GEMM or as per-expert
+ * dense GEMMs, and the weighted combine, for one GPU's share of experts.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensor pointers are DEVICE pointers owned by the caller; the library
+ *   never frees or retains them.  moe_dims and moe_opts live in host memory.
+ * - Layouts are row-major and dense.  bf16 tensors are passed as their
+ *   16-bit patterns (moe_bf16).  Expert weights use the [out, in] layout of
+ *   a linear layer, so both GEMM operands are contiguous along the reduced
+ *   dimension:  w_gate, w_up [EL][I][H];  w_down [EL][H][I];  shared
+ *   gate/up [Is][H], shared down [H][Is].
+ * - Every call is asynchronous on `stream` (a hipStream_t; NULL is the null
+ *   stream) unless stated otherwise.
+ * - Arguments are checked on the host before anything is enqueued; a bad
+ *   argument returns MOE_ERR_INVALID / MOE_ERR_UNSUPPORTED /
+ *   MOE_ERR_WORKSPACE and leaves every buffer untouched.  A failing HIP call
+ *   returns MOE_ERR_HIP.  moe_last_error() gives the message of the last
+ *   failure on the calling thread.  Nothing aborts or throws.
+ * - tokens == 0 is a valid no-op.
+ * - Supported sizes: 1 <= experts <= 256, 1 <= top_k <= min(experts, 8),
+ *   hidden, inter and shared_inter multiples of 64, local experts
+ *   [local_begin, local_begin + local_count) inside [0, experts),
+ *   tokens * top_k < 2^31.
+ * - Results are deterministic: the same inputs give the same bits on every
+ *   run, for any pipeline number and either GEMM kind.
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t moe_bf16; /* bf16 bit pattern */
+
+typedef enum {
+    MOE_OK = 0,
+    MOE_ERR_INVALID = 1,     /* null pointer, size out of range, bad option */
+    MOE_ERR_UNSUPPORTED = 2, /* experts > 256 or top_k > 8 */
+    MOE_ERR_WORKSPACE = 3,   /* workspace smaller than moe_workspace_bytes() */
+    MOE_ERR_HIP = 4          /* a HIP runtime call failed */
+} moe_status;
+
+/* Problem shape.  T tokens of width H are routed over E experts (top-k);
+ * this GPU computes local experts [local_begin, local_begin + local_count),
+ * each a SwiGLU FFN of width I, plus optional shared experts applied to
+ * every token whose concatenated width is shared_inter (0 = none). */
+typedef struct {
+    int64_t tokens;       /* T */
+    int32_t hidden;       /* H */
+    int32_t inter;        /* I */
+    int32_t experts;      /* E, router width */
+    int32_t top_k;        /* k */
+    int32_t local_begin;  /* e0 */
+    int32_t local_count;  /* EL */
+    int32_t renormalize;  /* 1: softmax over the k selected; 0: over all E */
+    int32_t shared_inter; /* Is (0 = no shared experts) */
+} moe_dims;
+
+enum { MOE_GEMM_AUTO = 0, MOE_GEMM_GROUP = 1, MOE_GEMM_DENSE = 2 };
+enum { MOE_FLAG_TIMING = 1 };
+
+/* Options of moe_ffn_forward (Sec. 4.3 of the paper: the GroupGemm /
+ * DenseGemm switch by load and the pipeline number PN). */
+typedef struct {
+    int32_t gemm_mode;      /* MOE_GEMM_AUTO, _GROUP or _DENSE */
+    int32_t dense_min_rows; /* AUTO picks DenseGemm for a pipeline stage when
+                               its experts average at least this many rows;
+                               0 = built-in default measured on MI355X */
+    int32_t pipeline_n;     /* PN >= 1, must divide local_count: stage s owns
+                               local experts [s*EL/PN, (s+1)*EL/PN) */
+    int32_t gemm_cu_budget; /* workgroups of the persistent grouped GEMM;
+                               0 = one per compute unit */
+    int32_t flags;          /* MOE_FLAG_TIMING: time each phase with HIP
+                               events (read with moe_last_timing) */
+    int32_t reserved[3];    /* must be zero */
+} moe_opts;
+
+/* Per-phase device time of the last moe_ffn_forward call on this thread
+ * that had MOE_FLAG_TIMING set, in milliseconds, summed over stages. */
+typedef struct {
+    float route_ms, permute_ms, gather_ms, gateup_ms, down_ms, shared_ms,
+        combine_ms, total_ms;
+    int32_t gateup_launches, down_launches; /* GEMM kernel launches timed */
+    int32_t dense_stages, group_stages;     /* policy decisions taken */
+} moe_timing;
+
+/* Bytes of device workspace: with opts == NULL, what moe_permute needs;
+ * with opts != NULL, what moe_ffn_forward needs (a superset).  Host-only;
+ * never touches the GPU.  Returns 0 for invalid dims. */
+size_t moe_workspace_bytes(const moe_dims *dims, const moe_opts *opts);
+
+/* Router (the topKGating operator of Sec. 3.3; k of E experts per token as
+ * in Sec. 3.2).  For each token t:
+ *   z[e] = fp32 fused-multiply-add chain over h = 0..H-1 (ascending, from
+ *          +0) of x[t][h] * w_router[e][h], then + bias[e] (one fp32 add)
+ *   topk_ids[t][0..k)  the k largest z, by (z descending, e ascending);
+ *                      -0 and +0 are equal
+ *   topk_w[t][j]       softmax weight, computed in fp64 and rounded to fp32:
+ *                      over the k selected logits when renormalize, else
+ *                      over all E logits.
+ * x [T][H] bf16; w_router [E][H] fp32; bias [E] fp32 or NULL;
+ * topk_ids [T][k] int32 (global expert ids); topk_w [T][k] fp32.
+ * Logits are never materialised.  NaN logits are not supported. */
+moe_status moe_route(const moe_dims *dims, const moe_bf16 *x, const float *w_router,
+                     const float *bias, int32_t *topk_ids, float *topk_w, void *stream);
+
+/* Dispatch (Fig. 7a: each expert takes its tokens in ascending order;
+ * Sec. 4.3: inputs split by rows, weights by expert).  Rows are ordered by
+ * (local expert ascending, token ascending):
+ *   counts [EL]        rows of each local expert
+ *   offsets [EL+1]     exclusive prefix of counts (unpadded)
+ *   sorted_slot [R]    row -> slot t*k+j   (R = offsets[EL] <= T*min(k,EL);
+ *                      the buffer must hold T*min(k,EL) entries)
+ *   slot_row [T*k]     slot -> row, -1 when the slot's expert is not local
+ *   x_perm [R][H]      x_perm[r] = x[sorted_slot[r] / k]; may be NULL to
+ *                      build the indices only (then x may be NULL too)
+ * Deterministic: scan-based, no atomics decide an order.
+ * ws: device workspace of at least moe_workspace_bytes(dims, NULL) bytes. */
+moe_status moe_permute(const moe_dims *dims, const int32_t *topk_ids, const moe_bf16 *x,
+                       int32_t *counts, int32_t *offsets, int32_t *sorted_slot,
+                       int32_t *slot_row, moe_bf16 *x_perm, void *ws, size_t ws_bytes,
+                       void *stream);
+
+/* Gather of the rows of local experts [e_first, e_first + e_count) only:
+ * x_perm[r] = x[sorted_slot[r] / k] for r in [offsets[e_first],
+ * offsets[e_first + e_count]).  offsets and sorted_slot are device arrays
+ * from moe_permute.  The dispatch of one pipeline stage. */
+moe_status moe_gather(const moe_dims *dims, int32_t e_first, int32_t e_count,
+                      const int32_t *offsets, const int32_t *sorted_slot,
+                      const moe_bf16 *x, moe_bf16 *x_perm, void *stream);
+
+/* GroupGemm expert FFN (Sec. 3.2, Conclusions 1-3; Fig. 3): ONE launch per
+ * GEMM for all rows of local experts [e_first, e_first + e_count), each
+ * expert with its own row count read on the device from offsets, so no
+ * host synchronisation is needed.  For every such row r of expert e:
+ *   act[r]    = bf16( silu(g) * u ), g = w_gate[e] x_perm[r],
+ *                                     u = w_up[e] x_perm[r]   (fp32 accum)
+ *   y_perm[r] = w_down[e] act[r]                               (fp32 accum)
+ * bf16 MFMA with fp32 accumulation; silu(g) = g / (1 + exp(-g)).
+ * w_gate/w_up/w_down point at the stacks of all EL local experts.
+ * act [R][I] bf16 (caller scratch, rows indexed like x_perm);
+ * y_perm [R][H] fp32.  cu_budget: persistent grid size (0 = all CUs). */
+moe_status moe_ffn_group(const moe_dims *dims, int32_t e_first, int32_t e_count,
+                         const int32_t *offsets, const moe_bf16 *x_perm,
+                         const moe_bf16 *w_gate, const moe_bf16 *w_up,
+                         const moe_bf16 *w_down, moe_bf16 *act, float *y_perm,
+                         int32_t cu_budget, void *stream);
+
+/* DenseGemm expert FFN (Sec. 4.3: with one expert per pipeline stage the
+ * grouped GEMM becomes a dense one): one dense SwiGLU FFN over `rows`
+ * contiguous rows whose count is known on the host:
+ *   act[r] = bf16(silu(w_gate x[r]) * (w_up x[r])),  y[r] = w_down act[r]
+ * x [rows][hidden] bf16; w_gate, w_up [inter][hidden]; w_down
+ * [hidden][inter]; act [rows][inter] bf16 scratch; y [rows][hidden] fp32.
+ * Also used for the shared experts (inter = shared width, x = all tokens).
+ * Same arithmetic and bits as moe_ffn_group for the same rows. */
+moe_status moe_ffn_dense(int64_t rows, int32_t hidden, int32_t inter, const moe_bf16 *x,
+                         const moe_bf16 *w_gate, const moe_bf16 *w_up,
+                         const moe_bf16 *w_down, moe_bf16 *act, float *y, void *stream);
+
+/* Combine (LocalReduce, Fig. 7b) of the local experts [e_first,
+ * e_first + e_count):  for every token t,
+ *   y[t] = (accumulate ? y[t] : 0) + sum_j topk_w[t][j] * y_perm[slot_row[t*k+j]]
+ * over the slots j whose expert lies in that range, the terms taken in
+ * ascending expert order, each added with one fp32 fused multiply-add.
+ * Running the stages of a pipeline in order (first with accumulate = 0, or
+ * all with accumulate = 1 over a y that holds the shared experts' output)
+ * gives the same bits as one call over all local experts.
+ * y_perm [R][H] fp32; topk_ids, slot_row [T][k] int32; topk_w [T][k];
+ * y [T][H] fp32. */
+moe_status moe_combine(const moe_dims *dims, int32_t e_first, int32_t e_count,
+                       const float *y_perm, const int32_t *topk_ids, const int32_t *slot_row,
+                       const float *topk_w, float *y, int32_t accumulate, void *stream);
+
+/* The whole forward of one MoE layer's routed FFN for this GPU's experts:
+ * route -> dispatch -> per pipeline stage { gather ; GroupGemm or DenseGemm
+ * (picked per stage from its row counts, Sec. 3.2 Conclusion 1 and
+ * Sec. 4.3) ; combine }, with stage i+1's gather and stage i-1's combine
+ * running on their own streams beside stage i's GEMMs (the one-GPU form of
+ * the expert pipeline of Sec. 4.3-4.4).  The shared experts (if any) run
+ * first and write y; otherwise the first combine writes every token.
+ * topk_ids, topk_w, counts: optional outputs (NULL = keep them in the
+ * workspace).  shared_*: required iff dims->shared_inter > 0.
+ * ws: at least moe_workspace_bytes(dims, opts) bytes of device memory.
+ * Ordered after prior work on `stream` and finished on `stream`.  When the
+ * policy needs row counts on the host (gemm_mode != GROUP or PN > 1) the
+ * call blocks the host once on a 4*EL-byte device-to-host copy. */
+moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe_bf16 *x,
+                           const float *w_router, const float *bias,
+                           const moe_bf16 *w_gate, const moe_bf16 *w_up,
+                           const moe_bf16 *w_down, const moe_bf16 *shared_gate,
+                           const moe_bf16 *shared_up, const moe_bf16 *shared_down,
+                           float *y, int32_t *topk_ids, float *topk_w, int32_t *counts,
+                           void *ws, size_t ws_bytes, void *stream);
+
+/* Timing of the last timed moe_ffn_forward on this thread (waits for its
+ * events).  Returns MOE_ERR_INVALID when no timed call was made. */
+moe_status moe_last_timing(moe_timing *out);
+
+/* The dense-GEMM threshold (rows per expert) AUTO uses when
+ * dense_min_rows == 0. */
+int32_t moe_default_dense_min_rows(void);
+
+const char *moe_status_string(moe_status s);
+const char *moe_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_H */

@@ -46,6 +46,7 @@ def _load():
     lib.oracle_dispatch.restype = i64
     lib.oracle_expert_row.argtypes = [P, P, P, P, i32, i32, i32, P]
     lib.oracle_expert_rows.argtypes = [P, P, P, P, P, P, i32, i32, i32, i32, P]
+    lib.oracle_expert_row_list.argtypes = [P, P, P, i64, P, P, P, i32, i32, P]
     lib.oracle_moe_tokens.argtypes = [P, P, P, P, i64, i32, i32, i32, i32, i32,
                                       P, P, P, i32, i32, P, P, P, P]
     lib.oracle_combine.argtypes = [P, P, P, P, i64, i32, i32, P]
@@ -107,6 +108,20 @@ def expert_row(x_row_bits, w_gate, w_up, w_down, el):
     EL, I, H = w_gate.shape
     y = np.empty(H, np.float32)
     _load().oracle_expert_row(_p(x_row_bits), _p(w_gate), _p(w_up), _p(w_down), H, I, el, _p(y))
+    return y
+
+
+def expert_row_list(x_bits, tokens, experts, w_gate, w_up, w_down):
+    """FFN rows for (token, local expert) pairs -> fp32 [n, H]."""
+    x_bits = _c(x_bits, np.uint16)
+    tok = _c(tokens, np.int64)
+    el = _c(experts, np.int32)
+    assert tok.shape == el.shape
+    w_gate, w_up, w_down = (_c(a, np.uint16) for a in (w_gate, w_up, w_down))
+    EL, I, H = w_gate.shape
+    y = np.empty((len(tok), H), np.float32)
+    _load().oracle_expert_row_list(_p(x_bits), _p(tok), _p(el), len(tok), _p(w_gate),
+                                   _p(w_up), _p(w_down), H, I, _p(y))
     return y
 
 

@@ -193,6 +193,16 @@ void oracle_expert_rows(const uint16_t *x, const int32_t *sorted_slot, const int
     }
 }
 
+/* Selected rows: y_rows[n] = FFN of local expert el[n] applied to token
+ * tok[n] (any list of pairs, e.g. a sample of dispatched rows). */
+void oracle_expert_row_list(const uint16_t *x, const int64_t *tok, const int32_t *el,
+                            int64_t n_rows, const uint16_t *wg, const uint16_t *wu,
+                            const uint16_t *wd, int H, int I, float *y_rows) {
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t n = 0; n < n_rows; ++n)
+        oracle_expert_row(x + tok[n] * H, wg, wu, wd, H, I, el[n], y_rows + n * H);
+}
+
 /* ---- steps 5-6 for a subset of tokens ------------------------------------ */
 /* Output rows y_sel[n] = MoE FFN of token tok[n], given the routing of that
  * token (ids, w as produced by oracle_topk).  Shared experts: n_shared

@@ -1,0 +1,97 @@
+// Internal declarations shared by the HIP sources of libmoe.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "moe.h"
+
+namespace moe {
+
+using bf16_t = uint16_t;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kMaxExperts = 256;
+constexpr int kMaxTopK = 8;
+constexpr int kDimAlign = 64;  // hidden / inter multiple
+
+// Records `msg` as the calling thread's last error and returns `s`.
+moe_status fail(moe_status s, const char *fmt, ...);
+// Checks a HIP return code; on failure records it and returns MOE_ERR_HIP.
+moe_status hip_check(hipError_t e, const char *what);
+
+#define MOE_HIP(expr)                                              \
+    do {                                                           \
+        moe_status _s = ::moe::hip_check((expr), #expr);           \
+        if (_s != MOE_OK) return _s;                               \
+    } while (0)
+
+#define MOE_TRY(expr)                      \
+    do {                                   \
+        moe_status _s = (expr);            \
+        if (_s != MOE_OK) return _s;       \
+    } while (0)
+
+// Host-side validation of the dims every entry point uses.
+moe_status check_dims(const moe_dims *d);
+
+// Number of compute units of the current device (cached per device).
+int device_cu_count();
+
+// Workspace layout used by moe_permute and moe_ffn_forward.
+struct WsLayout {
+    size_t chunk_counts;  // int32 [nchunks][EL]
+    size_t chunk_base;    // int32 [nchunks][EL]
+    size_t slot_rank;     // int32 [T*k]
+    size_t ids;           // int32 [T*k]   (forward, when the caller passes none)
+    size_t weights;       // fp32  [T*k]
+    size_t counts;        // int32 [EL]
+    size_t offsets;       // int32 [EL+1]
+    size_t sorted_slot;   // int32 [Rcap]
+    size_t slot_row;      // int32 [T*k]
+    size_t x_perm;        // bf16  [Rcap][H]
+    size_t act;           // bf16  [Rcap][I]
+    size_t y_perm;        // fp32  [Rcap][H]
+    size_t shared_act;    // bf16  [T][Is]
+    size_t total;
+    int64_t nchunks;
+    int64_t rcap;
+};
+WsLayout ws_layout(const moe_dims *d, bool forward);
+
+// Permutation chunking: slots handled by one workgroup of the histogram pass.
+constexpr int kPermChunk = 1024;
+
+// ---- kernel launchers (stream-ordered, no host synchronisation) ----------
+hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
+                        int32_t *ids, float *w, hipStream_t s);
+hipError_t launch_permute(const moe_dims &d, const int32_t *ids, void *ws, const WsLayout &L,
+                          int32_t *counts, int32_t *offsets, int32_t *sorted_slot,
+                          int32_t *slot_row, hipStream_t s);
+hipError_t launch_gather(const moe_dims &d, int e_first, int e_count, const int32_t *offsets,
+                         const int32_t *sorted_slot, const bf16_t *x, bf16_t *x_perm,
+                         int64_t max_rows, hipStream_t s);
+hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, const float *y_perm,
+                          const int32_t *ids, const int32_t *slot_row, const float *w,
+                          float *y, int accumulate, hipStream_t s);
+// Grouped GEMMs over local experts [e_first, e_first+e_count) (rows from
+// device offsets).  max_rows bounds the rows of the range (for grid sizing
+// only; pass T*min(k,EL) when unknown).
+hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
+                               const int32_t *offsets, const bf16_t *x_perm,
+                               const bf16_t *w_gate, const bf16_t *w_up, bf16_t *act,
+                               int grid, hipStream_t s);
+hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
+                             const int32_t *offsets, const bf16_t *act,
+                             const bf16_t *w_down, float *y_perm, int grid, hipStream_t s);
+// Dense GEMMs over `rows` host-known contiguous rows.
+hipError_t launch_dense_gateup(int64_t rows, int H, int I, const bf16_t *x, const bf16_t *w_gate,
+                               const bf16_t *w_up, bf16_t *act, hipStream_t s);
+hipError_t launch_dense_down(int64_t rows, int H, int I, const bf16_t *act,
+                             const bf16_t *w_down, float *y, hipStream_t s);
+
+}  // namespace moe

@@ -1,0 +1,338 @@
+// moe_ffn_forward: routing, dispatch, per-stage GEMM selection and the
+// expert pipeline over HIP streams.
+//
+// Streams (per device, created once, default priority):
+//   caller stream s0 : route, dispatch indices, the host copy of counts
+//   sg (gather)      : stage i's row gather (the one-GPU stand-in for the
+//                      dispatch all2all of one expert group)
+//   sm (GEMM)        : shared experts, then each stage's expert GEMMs
+//   sc (combine)     : each stage's weighted combine, in stage order
+// Stage i's GEMMs wait for its gather; its combine waits for its GEMMs, so
+// gather(i+1) and combine(i-1) overlap GEMM(i).  A stage is an expert
+// group: local experts [i*EL/PN, (i+1)*EL/PN), whose rows are one contiguous
+// range of the expert-sorted buffers, so each expert's weights are read by
+// exactly one stage (the paper's horizontal split with weights split by
+// expert, Sec. 4.3).  The GEMM kind of each stage is chosen from its row
+// counts (GroupGemm for small loads, DenseGemm per expert for large ones).
+#include <algorithm>
+#include <mutex>
+#include <vector>
+
+#include "common.h"
+
+namespace moe {
+namespace {
+
+constexpr int32_t kDefaultDenseMinRows = 4096;
+
+enum Phase {
+    PH_ROUTE, PH_PERMUTE, PH_GATHER, PH_GATEUP, PH_DOWN, PH_SHARED, PH_COMBINE, PH_TOTAL, PH_N
+};
+
+struct DevState {
+    hipStream_t sg = nullptr, sm = nullptr, sc = nullptr;
+    std::vector<hipEvent_t> sync_ev;   // ordering events (no timing)
+    std::vector<hipEvent_t> time_ev;   // timing events
+    int32_t *pinned_counts = nullptr;  // host-visible copy of counts
+    bool ready = false;
+};
+
+std::mutex g_mu;
+std::vector<DevState> g_dev;
+
+moe_status ensure_events(std::vector<hipEvent_t> &pool, size_t n, unsigned flags) {
+    while (pool.size() < n) {
+        hipEvent_t e;
+        MOE_HIP(hipEventCreateWithFlags(&e, flags));
+        pool.push_back(e);
+    }
+    return MOE_OK;
+}
+
+moe_status get_state(DevState **out) {
+    int dev = 0;
+    MOE_HIP(hipGetDevice(&dev));
+    std::lock_guard<std::mutex> lock(g_mu);
+    if ((int)g_dev.size() <= dev) g_dev.resize(dev + 1);
+    DevState &st = g_dev[dev];
+    if (!st.ready) {
+        MOE_HIP(hipStreamCreateWithFlags(&st.sg, hipStreamNonBlocking));
+        MOE_HIP(hipStreamCreateWithFlags(&st.sm, hipStreamNonBlocking));
+        MOE_HIP(hipStreamCreateWithFlags(&st.sc, hipStreamNonBlocking));
+        MOE_HIP(hipHostMalloc((void **)&st.pinned_counts, sizeof(int32_t) * kMaxExperts,
+                              hipHostMallocDefault));
+        st.ready = true;
+    }
+    *out = &st;
+    return MOE_OK;
+}
+
+struct TimedSpan {
+    int phase;
+    hipEvent_t start, stop;
+};
+
+struct TimingRecord {
+    std::vector<TimedSpan> spans;
+    int gateup_launches = 0, down_launches = 0, dense_stages = 0, group_stages = 0;
+    bool valid = false;
+};
+thread_local TimingRecord g_timing;
+
+// Records spans into the calling thread's record when enabled.
+class Timer {
+   public:
+    Timer(DevState *st, bool on) : st_(st), on_(on) {}
+    // Starts a span of `phase` on stream s; returns its index (or -1).
+    moe_status begin(hipStream_t s, int phase, int *idx = nullptr) {
+        int &i = idx ? *idx : cur_;
+        i = -1;
+        if (!on_) return MOE_OK;
+        hipEvent_t a, b;
+        {
+            std::lock_guard<std::mutex> lock(g_mu);
+            MOE_TRY(ensure_events(st_->time_ev, used_ + 2, hipEventDefault));
+            a = st_->time_ev[used_];
+            b = st_->time_ev[used_ + 1];
+        }
+        used_ += 2;
+        MOE_HIP(hipEventRecord(a, s));
+        i = (int)g_timing.spans.size();
+        g_timing.spans.push_back({phase, a, b});
+        return MOE_OK;
+    }
+    moe_status end(hipStream_t s, int idx = -2) {
+        if (!on_) return MOE_OK;
+        const int i = idx == -2 ? cur_ : idx;
+        if (i < 0) return MOE_OK;
+        MOE_HIP(hipEventRecord(g_timing.spans[i].stop, s));
+        return MOE_OK;
+    }
+
+   private:
+    DevState *st_;
+    bool on_;
+    size_t used_ = 0;
+    int cur_ = -1;
+};
+
+moe_status check_opts(const moe_dims *d, const moe_opts *o) {
+    if (o->gemm_mode < MOE_GEMM_AUTO || o->gemm_mode > MOE_GEMM_DENSE)
+        return fail(MOE_ERR_INVALID, "gemm_mode %d unknown", o->gemm_mode);
+    if (o->dense_min_rows < 0) return fail(MOE_ERR_INVALID, "dense_min_rows < 0");
+    if (o->pipeline_n < 1 || d->local_count % o->pipeline_n)
+        return fail(MOE_ERR_INVALID, "pipeline_n %d must be >= 1 and divide local_count %d",
+                    o->pipeline_n, d->local_count);
+    if (o->gemm_cu_budget < 0) return fail(MOE_ERR_INVALID, "gemm_cu_budget < 0");
+    if (o->flags & ~MOE_FLAG_TIMING) return fail(MOE_ERR_INVALID, "unknown flags 0x%x", o->flags);
+    for (int i = 0; i < 3; ++i)
+        if (o->reserved[i]) return fail(MOE_ERR_INVALID, "reserved options must be zero");
+    return MOE_OK;
+}
+
+}  // namespace
+}  // namespace moe
+
+using namespace moe;
+
+extern "C" {
+
+int32_t moe_default_dense_min_rows(void) { return kDefaultDenseMinRows; }
+
+moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe_bf16 *x,
+                           const float *w_router, const float *bias,
+                           const moe_bf16 *w_gate, const moe_bf16 *w_up,
+                           const moe_bf16 *w_down, const moe_bf16 *shared_gate,
+                           const moe_bf16 *shared_up, const moe_bf16 *shared_down,
+                           float *y, int32_t *topk_ids, float *topk_w, int32_t *counts,
+                           void *ws, size_t ws_bytes, void *stream) {
+    MOE_TRY(check_dims(dims));
+    moe_opts defaults{};
+    defaults.pipeline_n = 1;
+    const moe_opts *o = opts ? opts : &defaults;
+    MOE_TRY(check_opts(dims, o));
+    const moe_dims &d = *dims;
+    if (d.tokens == 0) return MOE_OK;
+    if (!x || !w_router || !w_gate || !w_up || !w_down || !y)
+        return fail(MOE_ERR_INVALID, "moe_ffn_forward: NULL tensor");
+    const bool has_shared = d.shared_inter > 0;
+    if (has_shared && (!shared_gate || !shared_up || !shared_down))
+        return fail(MOE_ERR_INVALID, "moe_ffn_forward: shared_inter > 0 needs shared weights");
+    const WsLayout L = ws_layout(dims, true);
+    if (!ws || ws_bytes < L.total)
+        return fail(MOE_ERR_WORKSPACE, "moe_ffn_forward: workspace %zu < %zu bytes", ws_bytes,
+                    L.total);
+
+    char *base = static_cast<char *>(ws);
+    int32_t *ids = topk_ids ? topk_ids : reinterpret_cast<int32_t *>(base + L.ids);
+    float *wts = topk_w ? topk_w : reinterpret_cast<float *>(base + L.weights);
+    int32_t *cnt = counts ? counts : reinterpret_cast<int32_t *>(base + L.counts);
+    int32_t *off = reinterpret_cast<int32_t *>(base + L.offsets);
+    int32_t *sorted_slot = reinterpret_cast<int32_t *>(base + L.sorted_slot);
+    int32_t *slot_row = reinterpret_cast<int32_t *>(base + L.slot_row);
+    bf16_t *x_perm = reinterpret_cast<bf16_t *>(base + L.x_perm);
+    bf16_t *act = reinterpret_cast<bf16_t *>(base + L.act);
+    float *y_perm = reinterpret_cast<float *>(base + L.y_perm);
+    bf16_t *shared_act = reinterpret_cast<bf16_t *>(base + L.shared_act);
+
+    DevState *st = nullptr;
+    MOE_TRY(get_state(&st));
+    const int PN = o->pipeline_n;
+    const int EL = d.local_count;
+    const int per_stage = EL / PN;
+    {
+        std::lock_guard<std::mutex> lock(g_mu);
+        MOE_TRY(ensure_events(st->sync_ev, 3 * (size_t)PN + 4, hipEventDisableTiming));
+    }
+    hipEvent_t ev_fork = st->sync_ev[0], ev_counts = st->sync_ev[1], ev_done = st->sync_ev[2],
+               ev_start = st->sync_ev[3];
+    hipEvent_t *ev_g = &st->sync_ev[4], *ev_m = ev_g + PN;
+
+    const bool timing = (o->flags & MOE_FLAG_TIMING) != 0;
+    if (timing) g_timing = TimingRecord{};
+    Timer tm(st, timing);
+    hipStream_t s0 = (hipStream_t)stream;
+    const int H = d.hidden, I = d.inter;
+    const int64_t T = d.tokens;
+
+    int total_span = -1;
+    MOE_TRY(tm.begin(s0, PH_TOTAL, &total_span));
+    // shared experts: independent of routing, start at once on the GEMM stream
+    MOE_HIP(hipEventRecord(ev_start, s0));
+    MOE_HIP(hipStreamWaitEvent(st->sm, ev_start, 0));
+    if (has_shared) {
+        MOE_TRY(tm.begin(st->sm, PH_SHARED));
+        MOE_HIP(launch_dense_gateup(T, H, d.shared_inter, x, shared_gate, shared_up, shared_act,
+                                    st->sm));
+        MOE_HIP(launch_dense_down(T, H, d.shared_inter, shared_act, shared_down, y, st->sm));
+        MOE_TRY(tm.end(st->sm));
+    }
+
+    // routing and dispatch indices on the caller stream
+    MOE_TRY(tm.begin(s0, PH_ROUTE));
+    MOE_HIP(launch_route(d, x, w_router, bias, ids, wts, s0));
+    MOE_TRY(tm.end(s0));
+    MOE_TRY(tm.begin(s0, PH_PERMUTE));
+    MOE_HIP(launch_permute(d, ids, ws, L, cnt, off, sorted_slot, slot_row, s0));
+    MOE_TRY(tm.end(s0));
+
+    // GEMM kind per stage needs the row counts on the host
+    std::vector<int32_t> hc;
+    const bool need_counts = o->gemm_mode != MOE_GEMM_GROUP || PN > 1;
+    if (need_counts) {
+        MOE_HIP(hipMemcpyAsync(st->pinned_counts, cnt, sizeof(int32_t) * EL,
+                               hipMemcpyDeviceToHost, s0));
+        MOE_HIP(hipEventRecord(ev_counts, s0));
+        MOE_HIP(hipEventSynchronize(ev_counts));
+        hc.assign(st->pinned_counts, st->pinned_counts + EL);
+    }
+    const int32_t m_star = o->dense_min_rows > 0 ? o->dense_min_rows : kDefaultDenseMinRows;
+    int grid = o->gemm_cu_budget > 0 ? o->gemm_cu_budget : device_cu_count();
+    grid = std::max(8, (grid / 8) * 8);
+
+    MOE_HIP(hipEventRecord(ev_fork, s0));
+    MOE_HIP(hipStreamWaitEvent(st->sg, ev_fork, 0));
+    MOE_HIP(hipStreamWaitEvent(st->sm, ev_fork, 0));
+    MOE_HIP(hipStreamWaitEvent(st->sc, ev_fork, 0));
+
+    for (int i = 0; i < PN; ++i) {
+        const int ef = i * per_stage;
+        int64_t stage_rows = L.rcap;
+        bool dense = o->gemm_mode == MOE_GEMM_DENSE;
+        if (need_counts) {
+            stage_rows = 0;
+            for (int e = ef; e < ef + per_stage; ++e) stage_rows += hc[e];
+            if (o->gemm_mode == MOE_GEMM_AUTO)
+                dense = stage_rows >= (int64_t)m_star * per_stage;
+        }
+        // gather (dispatch of this expert group)
+        MOE_TRY(tm.begin(st->sg, PH_GATHER));
+        MOE_HIP(launch_gather(d, ef, per_stage, off, sorted_slot, x, x_perm, stage_rows, st->sg));
+        MOE_TRY(tm.end(st->sg));
+        MOE_HIP(hipEventRecord(ev_g[i], st->sg));
+
+        // expert GEMMs
+        MOE_HIP(hipStreamWaitEvent(st->sm, ev_g[i], 0));
+        if (dense) {
+            if (timing) ++g_timing.dense_stages;
+            int64_t r0 = 0;
+            for (int e = 0; e < ef; ++e) r0 += hc[e];
+            for (int e = ef; e < ef + per_stage; ++e) {
+                const int64_t rows = hc[e];
+                if (rows > 0) {
+                    const int64_t wo = (int64_t)e * I * H;
+                    MOE_TRY(tm.begin(st->sm, PH_GATEUP));
+                    MOE_HIP(launch_dense_gateup(rows, H, I, x_perm + r0 * H, w_gate + wo,
+                                                w_up + wo, act + r0 * I, st->sm));
+                    MOE_TRY(tm.end(st->sm));
+                    MOE_TRY(tm.begin(st->sm, PH_DOWN));
+                    MOE_HIP(launch_dense_down(rows, H, I, act + r0 * I, w_down + wo,
+                                              y_perm + r0 * H, st->sm));
+                    MOE_TRY(tm.end(st->sm));
+                    if (timing) {
+                        ++g_timing.gateup_launches;
+                        ++g_timing.down_launches;
+                    }
+                }
+                r0 += rows;
+            }
+        } else {
+            if (timing) ++g_timing.group_stages;
+            if (stage_rows > 0) {
+                MOE_TRY(tm.begin(st->sm, PH_GATEUP));
+                MOE_HIP(launch_group_gateup(d, ef, per_stage, off, x_perm, w_gate, w_up, act, grid,
+                                            st->sm));
+                MOE_TRY(tm.end(st->sm));
+                MOE_TRY(tm.begin(st->sm, PH_DOWN));
+                MOE_HIP(launch_group_down(d, ef, per_stage, off, act, w_down, y_perm, grid,
+                                          st->sm));
+                MOE_TRY(tm.end(st->sm));
+                if (timing) {
+                    ++g_timing.gateup_launches;
+                    ++g_timing.down_launches;
+                }
+            }
+        }
+        MOE_HIP(hipEventRecord(ev_m[i], st->sm));
+
+        // weighted combine of this expert group
+        MOE_HIP(hipStreamWaitEvent(st->sc, ev_m[i], 0));
+        MOE_TRY(tm.begin(st->sc, PH_COMBINE));
+        MOE_HIP(launch_combine(d, ef, per_stage, y_perm, ids, slot_row, wts, y,
+                               (i > 0 || has_shared) ? 1 : 0, st->sc));
+        MOE_TRY(tm.end(st->sc));
+    }
+    MOE_HIP(hipEventRecord(ev_done, st->sc));
+    MOE_HIP(hipStreamWaitEvent(s0, ev_done, 0));
+    MOE_TRY(tm.end(s0, total_span));
+    if (timing) g_timing.valid = true;
+    return MOE_OK;
+}
+
+moe_status moe_last_timing(moe_timing *out) {
+    if (!out) return fail(MOE_ERR_INVALID, "moe_last_timing: NULL");
+    if (!g_timing.valid) return fail(MOE_ERR_INVALID, "moe_last_timing: no timed call");
+    float ph[PH_N] = {0};
+    for (const TimedSpan &sp : g_timing.spans) {
+        MOE_HIP(hipEventSynchronize(sp.stop));
+        float ms = 0.f;
+        MOE_HIP(hipEventElapsedTime(&ms, sp.start, sp.stop));
+        ph[sp.phase] += ms;
+    }
+    *out = moe_timing{};
+    out->route_ms = ph[PH_ROUTE];
+    out->permute_ms = ph[PH_PERMUTE];
+    out->gather_ms = ph[PH_GATHER];
+    out->gateup_ms = ph[PH_GATEUP];
+    out->down_ms = ph[PH_DOWN];
+    out->shared_ms = ph[PH_SHARED];
+    out->combine_ms = ph[PH_COMBINE];
+    out->total_ms = ph[PH_TOTAL];
+    out->gateup_launches = g_timing.gateup_launches;
+    out->down_launches = g_timing.down_launches;
+    out->dense_stages = g_timing.dense_stages;
+    out->group_stages = g_timing.group_stages;
+    return MOE_OK;
+}
+
+}  // extern "C"

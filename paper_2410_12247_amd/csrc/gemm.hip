@@ -1,0 +1,420 @@
+// Expert GEMMs of the SwiGLU FFN on gfx950 bf16 MFMA (fp32 accumulation).
+//
+// Two launches per expert group (the paper's Gate, Up and Down GEMMs, with
+// the silu activation folded into the first):
+//   gate/up : act[r][j] = bf16( silu(g) * u ),  g = Wg[j].x[r], u = Wu[j].x[r]
+//   down    : y[r][h]   = Wd[h].act[r]                           (fp32 out)
+// Both operands are contiguous along the reduced dimension.  The MFMA is
+// fed the WEIGHT rows as its first (row) operand and the TOKEN rows as its
+// second (column) operand, so each lane ends up holding four consecutive
+// output features of one token row: a 16-byte fp32 store (down) or an
+// 8-byte bf16 store (gate/up), and for gate/up the matching gate and up
+// values sit in the same lane, so SiLU*mul needs no data movement.
+//
+// Workgroup tile: BN weight rows x BM token rows, 4 waves (2 x 2), each wave
+// (BN/2) x (BM/2) built from v_mfma_f32_16x16x32_bf16 with its accumulators
+// in AGPRs.  K advances BK per stage through NS LDS stages filled by
+// LDS-DMA loads, so the loads of the next NS-1 stages are in flight while a
+// stage is multiplied.  16-byte chunks of each LDS row are XOR-swizzled so
+// MFMA operand reads hit distinct banks.
+//
+// Two schedulers share that tile code and its arithmetic (so both give the
+// same bits for the same rows):
+//   dense : one launch per expert over host-known rows, one tile per
+//           workgroup ("DenseGemm").
+//   group : one persistent launch over a range of experts whose row counts
+//           are read on the device; workgroups walk a tile list spanning
+//           all experts ("GroupGemm").
+// Both map workgroups to tiles XCD by XCD (the hardware deals workgroups
+// round-robin over the 8 XCDs), so the tiles running on one XCD are
+// neighbours in (m, n) and share activation and weight rows in its L2.
+#include "common.h"
+
+namespace moe {
+namespace {
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void gbl_void_t;
+
+constexpr int NTHREADS = 256;
+constexpr int NXCD = 8;
+constexpr int GROUP_N = 8;  // n-tiles per super-column of the tile order
+
+// XOR swizzle of the 16-byte chunk index inside an LDS row, chosen so that
+// the 16 rows one MFMA operand read touches fall on distinct banks (LDS
+// serves b128 reads eight lanes at a time): 128-byte rows (BK 64) use
+// row & 7, 64-byte rows (BK 32) use (row >> 1) & 3.
+template <int BK>
+__device__ __forceinline__ int swz(int row) {
+    return BK == 64 ? (row & 7) : ((row >> 1) & 3);
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <int MODE, int BN, int BM, int BK, int NS>
+struct Cfg {
+    static constexpr int WN = 2, WM = 2;
+    static constexpr int WTN = BN / WN;  // weight rows per wave
+    static constexpr int WTM = BM / WM;  // token rows per wave
+    static constexpr int TN = WTN / 16;  // 16-row MFMA tiles along weights
+    static constexpr int TM = WTM / 16;  // 16-row MFMA tiles along tokens
+    static constexpr int CPR = BK / 8;   // 16-byte chunks per LDS row
+    static constexpr int RPI = 64 / CPR; // rows one wave-wide LDS-DMA fills
+    static constexpr int W_INSTR = BN / 4 / RPI;  // DMA instructions per wave per stage
+    static constexpr int X_INSTR = BM / 4 / RPI;
+    static constexpr int LPS = W_INSTR + X_INSTR;
+    static constexpr int STAGE_W = BN * BK;  // bf16 elements per stage
+    static constexpr int STAGE_X = BM * BK;
+    static constexpr int STAGE = STAGE_W + STAGE_X;
+    // output columns one tile covers: act columns (gate/up) or features (down)
+    static constexpr int BNOUT = MODE == 0 ? BN / 2 : BN;
+    static_assert((NS - 2) * LPS <= 63, "vmcnt range");
+    static_assert(BN % (4 * RPI) == 0 && BM % (4 * RPI) == 0, "DMA tiling");
+};
+
+struct TileArgs {
+    const bf16_t *w0;  // first weight row of the tile (gate rows, or down rows)
+    const bf16_t *w1;  // first up row (gate/up only)
+    int n_valid;       // weight rows valid from w0 (per half for gate/up)
+    const bf16_t *x;   // first token row of the tile
+    int m_valid;       // token rows valid from x
+    int K;
+    void *out;         // output element (first token row, first column)
+    int64_t ldo;       // output row stride in elements
+};
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    __bf16 ha = static_cast<__bf16>(a);
+    __bf16 hb = static_cast<__bf16>(b);
+    uint16_t ua = __builtin_bit_cast(uint16_t, ha);
+    uint16_t ub = __builtin_bit_cast(uint16_t, hb);
+    return (uint32_t)ua | ((uint32_t)ub << 16);
+}
+
+__device__ __forceinline__ float silu_mul(float g, float u) {
+    return g * __frcp_rn(1.0f + __expf(-g)) * u;
+}
+
+// One output tile.  Global -> LDS copies are wave-wide LDS-DMA loads
+// (global_load_lds_dwordx4: lane l's 16 bytes land at base + 16*l, no
+// registers involved); each wave fills its quarter of the weight and token
+// rows of a stage.  NS stages are in flight: stage kt+NS-1 is requested
+// while stage kt is multiplied, and a wave only waits (vmcnt) for the stage
+// it needs next.
+template <int MODE, int BN, int BM, int BK, int NS>
+__device__ __forceinline__ void run_tile(const TileArgs &a, bf16_t *smem) {
+    using C = Cfg<MODE, BN, BM, BK, NS>;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wn = wave % C::WN;
+    const int wm = wave / C::WN;
+    const int K = a.K;
+    const int nk = K / BK;
+
+    floatx4 acc[C::TN][C::TM];
+#pragma unroll
+    for (int t = 0; t < C::TN; ++t)
+#pragma unroll
+        for (int m = 0; m < C::TM; ++m) acc[t][m] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // ---- LDS-DMA assignment: this wave fills weight rows
+    //      [wave*BN/4, (wave+1)*BN/4) and token rows [wave*BM/4, ...).
+    const int drow = lane / C::CPR;                               // row within one DMA
+    const int dchunk = ((lane % C::CPR) ^ swz<BK>(drow)) * 8;     // logical k offset
+    const bf16_t *wsrc;
+    int wrow0;
+    if (MODE == 0) {
+        // waves 0..1 copy gate rows, waves 2..3 copy up rows
+        const bool up = wave >= 2;
+        wsrc = up ? a.w1 : a.w0;
+        wrow0 = (wave & 1) * (BN / 4);
+    } else {
+        wsrc = a.w0;
+        wrow0 = wave * (BN / 4);
+    }
+    int woff[C::W_INSTR];
+#pragma unroll
+    for (int i = 0; i < C::W_INSTR; ++i) {
+        const int r = min(wrow0 + i * C::RPI + drow, a.n_valid - 1);  // tails read a valid row
+        woff[i] = r * K + dchunk;
+    }
+    int xoff[C::X_INSTR];
+#pragma unroll
+    for (int i = 0; i < C::X_INSTR; ++i) {
+        const int r = min(wave * (BM / 4) + i * C::RPI + drow, a.m_valid - 1);
+        xoff[i] = r * K + dchunk;
+    }
+    const int w_lds = wave * (BN / 4) * BK;  // element offset of this wave's rows
+    const int x_lds = C::STAGE_W + wave * (BM / 4) * BK;
+
+    auto issue = [&](int stage, int k0) {
+        bf16_t *sb = smem + stage * C::STAGE;
+#pragma unroll
+        for (int i = 0; i < C::W_INSTR; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void_t *)(wsrc + woff[i] + k0),
+                                             (lds_void_t *)(sb + w_lds + i * C::RPI * BK), 16,
+                                             0, 0);
+#pragma unroll
+        for (int i = 0; i < C::X_INSTR; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void_t *)(a.x + xoff[i] + k0),
+                                             (lds_void_t *)(sb + x_lds + i * C::RPI * BK), 16,
+                                             0, 0);
+    };
+
+    // ---- fragment rows (LDS row of lane 0 of each 16-row MFMA tile)
+    int arow[C::TN];
+#pragma unroll
+    for (int t = 0; t < C::TN; ++t) {
+        if (MODE == 0) {
+            arow[t] = t < C::TN / 2 ? wn * (C::WTN / 2) + t * 16
+                                    : BN / 2 + wn * (C::WTN / 2) + (t - C::TN / 2) * 16;
+        } else {
+            arow[t] = wn * C::WTN + t * 16;
+        }
+    }
+    const int lrow = lane & 15;
+    const int lk = lane >> 4;  // which 8-wide k group of the 32-wide MFMA step
+    const int lsw = swz<BK>(lrow);
+
+    auto compute = [&](int stage) {
+        const bf16_t *sw = smem + stage * C::STAGE;
+        const bf16_t *sx = sw + C::STAGE_W;
+#pragma unroll
+        for (int s = 0; s < BK / 32; ++s) {
+            const int chunk = ((s * 4 + lk) ^ lsw) * 8;
+            bf16x8 af[C::TN], bfr[C::TM];
+#pragma unroll
+            for (int t = 0; t < C::TN; ++t)
+                af[t] = *reinterpret_cast<const bf16x8 *>(sw + (arow[t] + lrow) * BK + chunk);
+#pragma unroll
+            for (int m = 0; m < C::TM; ++m)
+                bfr[m] = *reinterpret_cast<const bf16x8 *>(
+                    sx + (wm * C::WTM + m * 16 + lrow) * BK + chunk);
+#pragma unroll
+            for (int m = 0; m < C::TM; ++m)
+#pragma unroll
+                for (int t = 0; t < C::TN; ++t)
+                    acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[t], bfr[m],
+                                                                        acc[t][m], 0, 0, 0);
+        }
+    };
+
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+        if (s < nk) issue(s, s * BK);
+    if (nk >= NS - 1) wait_vmcnt<(NS - 2) * C::LPS>(); else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+
+    for (int kt0 = 0; kt0 < nk; kt0 += NS) {
+#pragma unroll
+        for (int u = 0; u < NS; ++u) {
+            const int kt = kt0 + u;
+            if (kt < nk) {
+                const bool ahead = kt + NS - 1 < nk;
+                if (ahead) issue((u + NS - 1) % NS, (kt + NS - 1) * BK);
+                compute(u);
+                if (kt + 1 < nk) {
+                    if (ahead) wait_vmcnt<(NS - 2) * C::LPS>(); else wait_vmcnt<0>();
+                    __builtin_amdgcn_s_barrier();
+                }
+            }
+        }
+    }
+    __builtin_amdgcn_s_barrier();  // LDS free for the next tile of this workgroup
+
+    // ---- epilogue: lane holds output columns col..col+3 of token row `row`
+    const int lcol4 = (lane >> 4) * 4;
+    if (MODE == 0) {
+        bf16_t *out = reinterpret_cast<bf16_t *>(a.out);
+#pragma unroll
+        for (int t = 0; t < C::TN / 2; ++t) {
+            const int col = wn * (C::WTN / 2) + t * 16 + lcol4;
+#pragma unroll
+            for (int m = 0; m < C::TM; ++m) {
+                const int row = wm * C::WTM + m * 16 + lrow;
+                if (row < a.m_valid && col < a.n_valid) {
+                    const floatx4 g = acc[t][m];
+                    const floatx4 u = acc[t + C::TN / 2][m];
+                    uint2 v;
+                    v.x = pack_bf16x2(silu_mul(g[0], u[0]), silu_mul(g[1], u[1]));
+                    v.y = pack_bf16x2(silu_mul(g[2], u[2]), silu_mul(g[3], u[3]));
+                    *reinterpret_cast<uint2 *>(out + row * a.ldo + col) = v;
+                }
+            }
+        }
+    } else {
+        float *out = reinterpret_cast<float *>(a.out);
+#pragma unroll
+        for (int t = 0; t < C::TN; ++t) {
+            const int col = wn * C::WTN + t * 16 + lcol4;
+#pragma unroll
+            for (int m = 0; m < C::TM; ++m) {
+                const int row = wm * C::WTM + m * 16 + lrow;
+                if (row < a.m_valid && col < a.n_valid)
+                    *reinterpret_cast<floatx4 *>(out + row * a.ldo + col) = acc[t][m];
+            }
+        }
+    }
+}
+
+// Tile order inside one expert: super-columns of GROUP_N n-tiles, walked
+// row by row, so consecutive tiles share token rows and weight rows.
+__device__ __forceinline__ void decode_tile(int tau, int MT, int NT, int &mt, int &nt) {
+    const int per_sc = GROUP_N * MT;
+    const int sc = tau / per_sc;
+    const int r = tau - sc * per_sc;
+    const int width = min(GROUP_N, NT - sc * GROUP_N);
+    mt = r / width;
+    nt = sc * GROUP_N + (r - mt * width);
+}
+
+template <int MODE, int BN, int BM, int BK, int NS>
+__global__ __launch_bounds__(NTHREADS, 1) void dense_kernel(const bf16_t *__restrict__ x,
+                                                            int64_t rows, const bf16_t *w0,
+                                                            const bf16_t *w1, int N, int K,
+                                                            void *out, int64_t ldo, int MT,
+                                                            int NT) {
+    using C = Cfg<MODE, BN, BM, BK, NS>;
+    __shared__ __attribute__((aligned(16))) bf16_t smem[NS * C::STAGE];
+    const int per = gridDim.x / NXCD;
+    const int tau = (blockIdx.x % NXCD) * per + blockIdx.x / NXCD;
+    if (tau >= MT * NT) return;
+    int mt, nt;
+    decode_tile(tau, MT, NT, mt, nt);
+    TileArgs a;
+    const int64_t n0 = (int64_t)nt * C::BNOUT;
+    const int64_t m0 = (int64_t)mt * BM;
+    a.w0 = w0 + n0 * K;
+    a.w1 = MODE == 0 ? w1 + n0 * K : nullptr;
+    a.n_valid = (int)(N - n0);
+    a.x = x + m0 * K;
+    a.m_valid = (int)min<int64_t>(BM, rows - m0);
+    a.K = K;
+    a.ldo = ldo;
+    if (MODE == 0)
+        a.out = reinterpret_cast<bf16_t *>(out) + m0 * ldo + n0;
+    else
+        a.out = reinterpret_cast<float *>(out) + m0 * ldo + n0;
+    run_tile<MODE, BN, BM, BK, NS>(a, smem);
+}
+
+template <int MODE, int BN, int BM, int BK, int NS>
+__global__ __launch_bounds__(NTHREADS, 1) void group_kernel(
+    const int32_t *__restrict__ offsets, int e_first, int e_count, const bf16_t *__restrict__ x,
+    const bf16_t *w0s, const bf16_t *w1s, int64_t wstride, int N, int K, void *out,
+    int64_t ldo) {
+    using C = Cfg<MODE, BN, BM, BK, NS>;
+    __shared__ __attribute__((aligned(16))) bf16_t smem[NS * C::STAGE];
+    __shared__ int s_off[kMaxExperts + 1];
+    __shared__ int s_pre[kMaxExperts + 1];
+    const int tid = threadIdx.x;
+    const int NT = (N + C::BNOUT - 1) / C::BNOUT;
+
+    for (int i = tid; i <= e_count; i += NTHREADS) s_off[i] = offsets[e_first + i];
+    __syncthreads();
+    // tiles per expert, then an inclusive scan (Hillis-Steele over <= 256)
+    int mine = 0;
+    if (tid < e_count) mine = ((s_off[tid + 1] - s_off[tid] + BM - 1) / BM) * NT;
+    if (tid < kMaxExperts) s_pre[tid + 1] = mine;
+    if (tid == 0) s_pre[0] = 0;
+    __syncthreads();
+    for (int d = 1; d < kMaxExperts; d <<= 1) {
+        int v = 0;
+        if (tid < kMaxExperts && tid >= d) v = s_pre[tid + 1 - d];
+        __syncthreads();
+        if (tid < kMaxExperts) s_pre[tid + 1] += v;
+        __syncthreads();
+    }
+    const int total = s_pre[e_count];
+
+    const int G = gridDim.x;  // multiple of NXCD
+    const int slot = (blockIdx.x % NXCD) * (G / NXCD) + blockIdx.x / NXCD;
+    for (int tau = slot; tau < total; tau += G) {
+        // expert: last e with s_pre[e] <= tau
+        int lo = 0, hi = e_count - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_pre[mid] <= tau) lo = mid; else hi = mid - 1;
+        }
+        const int e = lo;
+        const int cnt = s_off[e + 1] - s_off[e];
+        const int MT = (cnt + BM - 1) / BM;
+        int mt, nt;
+        decode_tile(tau - s_pre[e], MT, NT, mt, nt);
+        const int64_t n0 = (int64_t)nt * C::BNOUT;
+        const int64_t r0 = (int64_t)s_off[e] + (int64_t)mt * BM;
+        TileArgs a;
+        const int64_t woffe = (int64_t)(e_first + e) * wstride;
+        a.w0 = w0s + woffe + n0 * K;
+        a.w1 = MODE == 0 ? w1s + woffe + n0 * K : nullptr;
+        a.n_valid = (int)(N - n0);
+        a.x = x + r0 * K;
+        a.m_valid = min(BM, cnt - mt * BM);
+        a.K = K;
+        a.ldo = ldo;
+        if (MODE == 0)
+            a.out = reinterpret_cast<bf16_t *>(out) + r0 * ldo + n0;
+        else
+            a.out = reinterpret_cast<float *>(out) + r0 * ldo + n0;
+        run_tile<MODE, BN, BM, BK, NS>(a, smem);
+    }
+}
+
+// Tile shapes: BN weight rows x BM token rows, BK k per stage, NS stages.
+constexpr int DENSE_BN = 256, DENSE_BM = 256, DENSE_BK = 32, DENSE_NS = 4;
+constexpr int GROUP_BN = 256, GROUP_BM = 256, GROUP_BK = 32, GROUP_NS = 4;
+#define DENSE_CFG DENSE_BN, DENSE_BM, DENSE_BK, DENSE_NS
+#define GROUP_CFG GROUP_BN, GROUP_BM, GROUP_BK, GROUP_NS
+
+int round_grid(int64_t tiles) { return (int)(((tiles + NXCD - 1) / NXCD) * NXCD); }
+
+}  // namespace
+
+hipError_t launch_dense_gateup(int64_t rows, int H, int I, const bf16_t *x, const bf16_t *w_gate,
+                               const bf16_t *w_up, bf16_t *act, hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    using C = Cfg<0, DENSE_CFG>;
+    const int MT = (int)((rows + DENSE_BM - 1) / DENSE_BM);
+    const int NT = (I + C::BNOUT - 1) / C::BNOUT;
+    dense_kernel<0, DENSE_CFG><<<round_grid((int64_t)MT * NT), NTHREADS, 0, s>>>(
+        x, rows, w_gate, w_up, I, H, act, I, MT, NT);
+    return hipGetLastError();
+}
+
+hipError_t launch_dense_down(int64_t rows, int H, int I, const bf16_t *act,
+                             const bf16_t *w_down, float *y, hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    using C = Cfg<1, DENSE_CFG>;
+    const int MT = (int)((rows + DENSE_BM - 1) / DENSE_BM);
+    const int NT = (H + C::BNOUT - 1) / C::BNOUT;
+    dense_kernel<1, DENSE_CFG><<<round_grid((int64_t)MT * NT), NTHREADS, 0, s>>>(
+        act, rows, w_down, nullptr, H, I, y, H, MT, NT);
+    return hipGetLastError();
+}
+
+hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
+                               const int32_t *offsets, const bf16_t *x_perm,
+                               const bf16_t *w_gate, const bf16_t *w_up, bf16_t *act,
+                               int grid, hipStream_t s) {
+    if (e_count <= 0) return hipSuccess;
+    group_kernel<0, GROUP_CFG><<<grid, NTHREADS, 0, s>>>(
+        offsets, e_first, e_count, x_perm, w_gate, w_up, (int64_t)d.inter * d.hidden, d.inter,
+        d.hidden, act, d.inter);
+    return hipGetLastError();
+}
+
+hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
+                             const int32_t *offsets, const bf16_t *act,
+                             const bf16_t *w_down, float *y_perm, int grid, hipStream_t s) {
+    if (e_count <= 0) return hipSuccess;
+    group_kernel<1, GROUP_CFG><<<grid, NTHREADS, 0, s>>>(
+        offsets, e_first, e_count, act, w_down, nullptr, (int64_t)d.hidden * d.inter, d.hidden,
+        d.inter, y_perm, d.hidden);
+    return hipGetLastError();
+}
+
+}  // namespace moe

@@ -1,0 +1,251 @@
+// Router: fp32 logits, top-k selection and softmax weights in one kernel.
+//
+// Logits (the topKGating operator): each lane owns one token and a wave owns
+// a quarter of the experts, so every logit is ONE fp32 fma chain over h in
+// ascending order, started from +0, with the bias added once at the end --
+// the same bits as a sequential fma loop on the CPU.  x and the router are
+// staged through LDS 32 h at a time; router reads are wave-wide broadcasts.
+//
+// Selection: the token's logits are spread over a wave (lane l holds experts
+// l, l+64, l+128, l+192); each of the k rounds is a wave-wide max of 64-bit
+// keys (order-preserving logit bits << 32 | inverted expert index, so ties
+// go to the lower index) built from DPP row permutes and readlane.  The
+// winner's lane clears its key.  Softmax weights are computed in fp64 and
+// rounded to fp32 once; the full-softmax denominator is a DPP wave sum.
+#include "common.h"
+
+namespace moe {
+namespace {
+
+constexpr int RT_TOK = 64;  // tokens per workgroup (one per lane)
+constexpr int RT_HC = 32;   // h per LDS chunk
+constexpr int RT_LD = RT_HC + 4;
+constexpr int RT_THREADS = 256;
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+    uint32_t lo = dpp32<CTRL>((uint32_t)v);
+    uint32_t hi = dpp32<CTRL>((uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+    uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Wave-wide max: butterfly inside each 16-lane row (quad_perm 1032, quad_perm
+// 2301, half-row mirror, row mirror), then the four row results by readlane.
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t k) {
+    k = max_u64(k, dpp64<0xB1>(k));
+    k = max_u64(k, dpp64<0x4E>(k));
+    k = max_u64(k, dpp64<0x141>(k));
+    k = max_u64(k, dpp64<0x140>(k));
+    return max_u64(max_u64(readlane64(k, 0), readlane64(k, 16)),
+                   max_u64(readlane64(k, 32), readlane64(k, 48)));
+}
+
+__device__ __forceinline__ double dpp_f64(double v, int which) {
+    uint64_t b = __builtin_bit_cast(uint64_t, v);
+    uint64_t r;
+    switch (which) {
+        case 0: r = dpp64<0xB1>(b); break;
+        case 1: r = dpp64<0x4E>(b); break;
+        case 2: r = dpp64<0x141>(b); break;
+        default: r = dpp64<0x140>(b); break;
+    }
+    return __builtin_bit_cast(double, r);
+}
+
+// Wave-wide fp64 sum; every lane combines the same pairs (commutative adds),
+// so the result is identical in all lanes and from run to run.
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v = v + dpp_f64(v, i);
+    uint64_t b = __builtin_bit_cast(uint64_t, v);
+    double r0 = __builtin_bit_cast(double, readlane64(b, 0));
+    double r1 = __builtin_bit_cast(double, readlane64(b, 16));
+    double r2 = __builtin_bit_cast(double, readlane64(b, 32));
+    double r3 = __builtin_bit_cast(double, readlane64(b, 48));
+    return (r0 + r1) + (r2 + r3);
+}
+
+__device__ __forceinline__ uint64_t logit_key(float z, int e) {
+    uint32_t u = __float_as_uint(z);
+    if (u == 0x80000000u) u = 0;  // -0 ranks equal to +0
+    const uint32_t ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ((uint64_t)ord << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)e);
+}
+
+__device__ __forceinline__ float key_logit(uint64_t key) {
+    const uint32_t ord = (uint32_t)(key >> 32);
+    const uint32_t u = (ord & 0x80000000u) ? (ord & 0x7FFFFFFFu) : ~ord;
+    return __uint_as_float(u);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// RE: maximum experts per wave (E <= 4*RE).
+template <int RE>
+__global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restrict__ x,
+                                                           const float *__restrict__ wr,
+                                                           const float *__restrict__ bias,
+                                                           int64_t T, int H, int E, int k,
+                                                           int renorm, int32_t *__restrict__ ids,
+                                                           float *__restrict__ wout) {
+    constexpr int EMAX = 4 * RE;
+    constexpr int P1 = RT_TOK * RT_LD + EMAX * RT_LD;  // floats, logits phase
+    constexpr int P2 = RT_TOK * (EMAX + 1);            // floats, selection phase
+    __shared__ __attribute__((aligned(16))) float lds[P1 > P2 ? P1 : P2];
+    float *xs = lds;                  // [RT_TOK][RT_LD]
+    float *ws = lds + RT_TOK * RT_LD; // [E][RT_LD]
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int g = tid >> 6;                 // wave: experts [g*re, g*re + re)
+    const int re = (E + 3) / 4;
+    const int ebase = g * re;
+    const int64_t t0 = (int64_t)blockIdx.x * RT_TOK;
+
+    float acc[RE];
+#pragma unroll
+    for (int j = 0; j < RE; ++j) acc[j] = 0.0f;
+
+    const int xtok = tid >> 2, xpart = tid & 3;
+    const int64_t xt = min<int64_t>(t0 + xtok, T - 1);
+    const bf16_t *xrow = x + xt * H + xpart * 8;
+
+    for (int h0 = 0; h0 < H; h0 += RT_HC) {
+        {
+            const uint4 v = *reinterpret_cast<const uint4 *>(xrow + h0);
+            float4 a = make_float4(bf16_lo(v.x), bf16_hi(v.x), bf16_lo(v.y), bf16_hi(v.y));
+            float4 b = make_float4(bf16_lo(v.z), bf16_hi(v.z), bf16_lo(v.w), bf16_hi(v.w));
+            *reinterpret_cast<float4 *>(xs + xtok * RT_LD + xpart * 8) = a;
+            *reinterpret_cast<float4 *>(xs + xtok * RT_LD + xpart * 8 + 4) = b;
+        }
+        for (int c = tid; c < E * 8; c += RT_THREADS) {
+            const int e = c >> 3, part = c & 7;
+            *reinterpret_cast<float4 *>(ws + e * RT_LD + part * 4) =
+                *reinterpret_cast<const float4 *>(wr + (int64_t)e * H + h0 + part * 4);
+        }
+        __syncthreads();
+#pragma unroll 2
+        for (int hh = 0; hh < RT_HC; hh += 4) {
+            const float4 xv = *reinterpret_cast<const float4 *>(xs + lane * RT_LD + hh);
+#pragma unroll
+            for (int j = 0; j < RE; ++j) {
+                if (j < re && ebase + j < E) {
+                    const float4 wv =
+                        *reinterpret_cast<const float4 *>(ws + (ebase + j) * RT_LD + hh);
+                    float a = acc[j];
+                    a = __builtin_fmaf(xv.x, wv.x, a);
+                    a = __builtin_fmaf(xv.y, wv.y, a);
+                    a = __builtin_fmaf(xv.z, wv.z, a);
+                    a = __builtin_fmaf(xv.w, wv.w, a);
+                    acc[j] = a;
+                }
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- logits to LDS: zs[token][e], row stride EMAX+1 (odd: no conflicts)
+    float *zs = lds;
+    constexpr int ZLD = EMAX + 1;
+#pragma unroll
+    for (int j = 0; j < RE; ++j) {
+        const int e = ebase + j;
+        if (j < re && e < E) {
+            float z = acc[j];
+            if (bias) z = z + bias[e];
+            zs[lane * ZLD + e] = z;
+        }
+    }
+    __syncthreads();
+
+    // ---- selection: wave g handles tokens [g*16, g*16+16)
+    for (int tt = g * 16; tt < g * 16 + 16; ++tt) {
+        const int64_t t = t0 + tt;
+        if (t >= T) break;
+        uint64_t key[4];
+        float zl[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = lane + 64 * q;
+            zl[q] = e < E ? zs[tt * ZLD + e] : 0.0f;
+            key[q] = e < E ? logit_key(zl[q], e) : 0ull;
+        }
+        int sel_e[kMaxTopK];
+        float sel_z[kMaxTopK];
+#pragma unroll
+        for (int j = 0; j < kMaxTopK; ++j) {
+            sel_e[j] = 0;
+            sel_z[j] = 0.0f;
+            if (j < k) {
+                const uint64_t best =
+                    wave_max_u64(max_u64(max_u64(key[0], key[1]), max_u64(key[2], key[3])));
+                sel_e[j] = (int)(0xFFFFFFFFu - (uint32_t)best);
+                sel_z[j] = key_logit(best);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (key[q] == best) key[q] = 0ull;
+            }
+        }
+        const double zmax = (double)sel_z[0];
+        double denom;
+        if (renorm) {
+            denom = 0.0;
+#pragma unroll
+            for (int j = 0; j < kMaxTopK; ++j)
+                if (j < k) denom += exp((double)sel_z[j] - zmax);
+        } else {
+            double part = 0.0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (lane + 64 * q < E) part += exp((double)zl[q] - zmax);
+            denom = wave_sum_f64(part);
+        }
+#pragma unroll
+        for (int j = 0; j < kMaxTopK; ++j) {
+            if (j < k && lane == j) {
+                ids[t * k + j] = sel_e[j];
+                wout[t * k + j] = (float)(exp((double)sel_z[j] - zmax) / denom);
+            }
+        }
+    }
+}
+
+template <int RE>
+hipError_t launch_re(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
+                     int32_t *ids, float *w, hipStream_t s) {
+    const int64_t blocks = (d.tokens + RT_TOK - 1) / RT_TOK;
+    route_kernel<RE><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
+        x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
+                        int32_t *ids, float *w, hipStream_t s) {
+    if (d.tokens <= 0) return hipSuccess;
+    const int re = (d.experts + 3) / 4;
+    if (re <= 2) return launch_re<2>(d, x, wr, bias, ids, w, s);
+    if (re <= 4) return launch_re<4>(d, x, wr, bias, ids, w, s);
+    if (re <= 8) return launch_re<8>(d, x, wr, bias, ids, w, s);
+    if (re <= 16) return launch_re<16>(d, x, wr, bias, ids, w, s);
+    if (re <= 32) return launch_re<32>(d, x, wr, bias, ids, w, s);
+    if (re <= 48) return launch_re<48>(d, x, wr, bias, ids, w, s);
+    return launch_re<64>(d, x, wr, bias, ids, w, s);
+}
+
+}  // namespace moe

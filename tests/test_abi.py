@@ -1,0 +1,123 @@
+"""CPU checks of the C-ABI library: it loads, exports what include/moe.h
+declares, sizes workspaces on the host, and rejects bad arguments before any
+GPU work (so these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2410_12247_amd import moe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    L = moe.lib()
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(L, n), f"libmoe.so does not export {n}"
+    assert set(names) == set(moe.EXPORTS)
+
+
+def test_status_strings():
+    L = moe.lib()
+    assert L.moe_status_string(0) == b"ok"
+    assert L.moe_status_string(3) == b"workspace too small"
+
+
+def test_workspace_bytes_host_only():
+    d = moe.dims(16384, 4096, 3584, 8, 2)
+    fw = moe.workspace_bytes(d, moe.opts())
+    pm = moe.workspace_bytes(d)
+    assert 0 < pm < fw
+    R = 16384 * 2
+    # forward workspace holds x_perm (bf16), act (bf16) and y_perm (fp32) rows
+    assert fw >= R * (4096 * 2 + 3584 * 2 + 4096 * 4)
+    assert moe.workspace_bytes(moe.dims(16, 100, 64, 8, 2), moe.opts()) == 0  # H % 64
+
+
+BAD = [
+    (dict(tokens=-1), 1),
+    (dict(hidden=100), 1),
+    (dict(inter=0), 1),
+    (dict(experts=300), 2),
+    (dict(top_k=9), 2),
+    (dict(top_k=0), 1),
+    (dict(top_k=5, experts=4), 1),
+    (dict(local_begin=6, local_count=4), 1),
+    (dict(local_count=0), 1),
+    (dict(renormalize=2), 1),
+    (dict(shared_inter=96), 1),
+    (dict(tokens=1 << 29, top_k=8), 1),
+]
+
+
+@pytest.mark.parametrize("change,status", BAD)
+def test_invalid_dims_rejected_before_any_gpu_work(change, status):
+    base = dict(tokens=64, hidden=256, inter=128, experts=8, top_k=2, local_begin=0,
+                local_count=8, renormalize=1, shared_inter=0)
+    base.update(change)
+    d = moe.Dims(**base)
+    fake = ctypes.c_void_p(16)  # never dereferenced: validation fails first
+    L = moe.lib()
+    st = L.moe_route(ctypes.byref(d), fake, fake, None, fake, fake, None)
+    assert st == status, L.moe_last_error()
+    assert L.moe_last_error()
+    st = L.moe_ffn_forward(ctypes.byref(d), None, fake, fake, None, fake, fake, fake, None,
+                           None, None, fake, None, None, None, fake, 1 << 40, None)
+    assert st == status
+
+
+def test_invalid_options_and_buffers_rejected():
+    L = moe.lib()
+    d = moe.dims(64, 256, 128, 8, 2)
+    fake = ctypes.c_void_p(16)
+    for o in (moe.opts(pipeline_n=3), moe.opts(pipeline_n=0), moe.opts(gemm_mode=7),
+              moe.opts(gemm_cu_budget=-1)):
+        st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake,
+                               fake, None, None, None, fake, None, None, None, fake, 1 << 40,
+                               None)
+        assert st == 1, L.moe_last_error()
+    o = moe.opts()
+    o.reserved[1] = 5
+    st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake, fake,
+                           None, None, None, fake, None, None, None, fake, 1 << 40, None)
+    assert st == 1
+    # workspace too small
+    st = L.moe_ffn_forward(ctypes.byref(d), None, fake, fake, None, fake, fake, fake, None,
+                           None, None, fake, None, None, None, fake, 10, None)
+    assert st == 3
+    # NULL required tensors
+    st = L.moe_route(ctypes.byref(d), None, fake, None, fake, fake, None)
+    assert st == 1
+    # shared experts declared but not given
+    ds = moe.dims(64, 256, 128, 8, 2, shared_inter=128)
+    st = L.moe_ffn_forward(ctypes.byref(ds), None, fake, fake, None, fake, fake, fake, None,
+                           None, None, fake, None, None, None, fake, 1 << 40, None)
+    assert st == 1
+    # expert ranges
+    assert L.moe_gather(ctypes.byref(d), 6, 3, fake, fake, fake, fake, None) == 1
+    assert L.moe_combine(ctypes.byref(d), 0, 9, fake, fake, fake, fake, fake, 0, None) == 1
+    assert L.moe_combine(ctypes.byref(d), 0, 8, fake, fake, fake, fake, fake, 2, None) == 1
+    assert L.moe_ffn_group(ctypes.byref(d), -1, 2, fake, fake, fake, fake, fake, fake, fake, 0,
+                           None) == 1
+    assert L.moe_ffn_dense(10, 100, 64, fake, fake, fake, fake, fake, fake, None) == 1
+    assert L.moe_last_timing(None) == 1
+
+
+def test_zero_token_calls_are_noops_on_the_host():
+    L = moe.lib()
+    d = moe.dims(0, 256, 128, 8, 2)
+    assert L.moe_route(ctypes.byref(d), None, None, None, None, None, None) == 0
+    assert L.moe_permute(ctypes.byref(d), None, None, None, None, None, None, None, None, 0,
+                         None) == 0
+    assert L.moe_ffn_dense(0, 256, 128, None, None, None, None, None, None, None) == 0

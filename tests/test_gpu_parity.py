@@ -1,0 +1,236 @@
+"""GPU parity of every step of the routed MoE FFN against the CPU oracle, at
+sizes the oracle finishes in seconds that still span several GEMM tiles and
+ragged tails.  All calls go through the C-ABI (libmoe.so)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2410_12247_amd import moe, synth
+
+from gpu_util import Dev, assert_close, bf16, bits, dev, f32, i32
+
+pytestmark = pytest.mark.gpu
+
+C = synth.custom_shape
+CASES = {
+    # the tiny workload in full
+    "tiny": synth.SHAPES["tiny"],
+    # ragged: H = 5*64, I = 3*64 (partial gate/up and down tiles), T not a
+    # multiple of any tile
+    "ragged8": C(name="ragged8", index=201, T=1000, H=320, I=192, E=8, EL=8, k=2, renorm=True),
+    # a local window [3, 8) of 16 experts, top-4
+    "window": C(name="window", index=202, T=777, H=512, I=384, E=16, EL=5, e0=3, k=4,
+                renorm=True),
+    # DeepSeekV2-like: 20 of 160 local, top-6 without renorm, shared experts
+    "fine": C(name="fine", index=203, T=333, H=256, I=128, E=160, EL=20, k=6, renorm=False,
+              n_shared=2, Is=128),
+    # k == E
+    "k_eq_E": C(name="k_eq_E", index=204, T=64, H=128, I=64, E=6, EL=6, k=6, renorm=False),
+    # a single token
+    "one": C(name="one", index=205, T=1, H=256, I=256, E=8, EL=8, k=2, renorm=True),
+}
+
+_cache = {}
+
+
+def case(name):
+    if name not in _cache:
+        inp = synth.make_inputs(CASES[name])
+        _, ids, w = oracle.route(inp.x, inp.w_router, inp.bias, inp.shape.k, inp.shape.renorm)
+        _cache[name] = (inp, ids, w)
+    return _cache[name]
+
+
+def oracle_y(inp, ids, w, tokens):
+    s = inp.shape
+    return oracle.moe_tokens(inp.x, ids, w, tokens, inp.w_gate, inp.w_up, inp.w_down, s.e0,
+                             s.n_shared, inp.shared_gate, inp.shared_up, inp.shared_down)
+
+
+def weights_match(got, ref):
+    # fp64 softmax rounded once on both sides; allow one fp32 ulp
+    return np.all(np.abs(got.astype(np.float64) - ref) <= 2.0 ** -23 * np.abs(ref) + 1e-30)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_route(name):
+    inp, ids, w = case(name)
+    g = Dev(inp)
+    s = inp.shape
+    gids = torch.empty((s.T, s.k), dtype=torch.int32, device=dev())
+    gw = torch.empty((s.T, s.k), dtype=torch.float32, device=dev())
+    moe.route(g.d, g.x, g.w_router, g.bias, gids, gw)
+    torch.cuda.synchronize()
+    assert np.array_equal(gids.cpu().numpy(), ids)
+    assert weights_match(gw.cpu().numpy(), w)
+
+
+def test_route_ties_and_signed_zero():
+    """Exact ties in the logits (duplicated router rows, zero rows) must go to
+    the lower expert index, -0 and +0 being equal."""
+    rng = np.random.default_rng(9)
+    T, H, E, k = 300, 64, 12, 4
+    xb = synth.bf16_bits(rng.standard_normal((T, H), dtype=np.float32))
+    wr = rng.standard_normal((E, H), dtype=np.float32) * np.float32(0.1)
+    wr[5] = wr[2]
+    wr[9] = wr[2]
+    wr[7] = 0.0
+    wr[3] = 0.0
+    xb[:20] = synth.bf16_bits(np.zeros((20, H), np.float32))  # all logits +0
+    xb[20:40] = synth.bf16_bits(-np.zeros((20, H), np.float32))
+    _, ids, w = oracle.route(xb, wr, None, k, True)
+    d = moe.dims(T, H, 64, E, k)
+    gids = torch.empty((T, k), dtype=torch.int32, device=dev())
+    gw = torch.empty((T, k), dtype=torch.float32, device=dev())
+    moe.route(d, bf16(xb), f32(wr), None, gids, gw)
+    torch.cuda.synchronize()
+    assert np.array_equal(gids.cpu().numpy(), ids)
+    assert weights_match(gw.cpu().numpy(), w)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_permute_and_gather(name):
+    inp, ids, _ = case(name)
+    s = inp.shape
+    g = Dev(inp)
+    counts, offsets, sorted_slot, slot_row = oracle.dispatch(ids, s.e0, s.EL)
+    rcap = s.T * min(s.k, s.EL)
+    gc = torch.empty(s.EL, dtype=torch.int32, device=dev())
+    go = torch.empty(s.EL + 1, dtype=torch.int32, device=dev())
+    gss = torch.full((rcap,), -7, dtype=torch.int32, device=dev())
+    gsr = torch.empty(s.T * s.k, dtype=torch.int32, device=dev())
+    gxp = torch.empty((rcap, s.H), dtype=torch.bfloat16, device=dev())
+    ws = torch.empty(moe.workspace_bytes(g.d), dtype=torch.uint8, device=dev())
+    moe.permute(g.d, i32(ids), g.x, gc, go, gss, gsr, gxp, ws)
+    torch.cuda.synchronize()
+    R = int(offsets[-1])
+    assert np.array_equal(gc.cpu().numpy(), counts)
+    assert np.array_equal(go.cpu().numpy(), offsets)
+    assert np.array_equal(gss.cpu().numpy()[:R], sorted_slot)
+    assert np.array_equal(gsr.cpu().numpy(), slot_row)
+    assert np.array_equal(bits(gxp[:R]), inp.x[sorted_slot // s.k])
+
+
+@pytest.mark.parametrize("name", ["tiny", "ragged8", "window", "fine"])
+def test_ffn_group_and_dense_rows(name):
+    """GroupGemm over all local experts and DenseGemm per expert: every
+    dispatched row against the oracle's expert FFN, and the two GEMM kinds
+    bit-identical."""
+    inp, ids, _ = case(name)
+    s = inp.shape
+    g = Dev(inp)
+    counts, offsets, sorted_slot, _ = oracle.dispatch(ids, s.e0, s.EL)
+    R = int(offsets[-1])
+    xp = inp.x[sorted_slot // s.k]
+    gxp = bf16(xp) if R else torch.empty((0, s.H), dtype=torch.bfloat16, device=dev())
+    act = torch.empty((max(R, 1), s.I), dtype=torch.bfloat16, device=dev())
+    yg = torch.full((max(R, 1), s.H), float("nan"), dtype=torch.float32, device=dev())
+    moe.ffn_group(g.d, 0, s.EL, i32(offsets), gxp if R else act, g.w_gate, g.w_up,
+                  g.w_down, act, yg)
+    yd = torch.full((max(R, 1), s.H), float("nan"), dtype=torch.float32, device=dev())
+    act_d = torch.empty_like(act)
+    for e in range(s.EL):
+        r0, r1 = int(offsets[e]), int(offsets[e + 1])
+        if r1 > r0:
+            moe.ffn_dense(r1 - r0, s.H, s.I, gxp[r0:r1], g.w_gate[e], g.w_up[e], g.w_down[e],
+                          act_d[r0:r1], yd[r0:r1])
+    torch.cuda.synchronize()
+    experts = np.repeat(np.arange(s.EL), counts)
+    ref = oracle.expert_row_list(inp.x, sorted_slot // s.k, experts, inp.w_gate, inp.w_up,
+                                 inp.w_down)
+    got_g = yg.cpu().numpy()[:R]
+    assert_close(got_g, ref, f"{name} group rows")
+    assert np.array_equal(got_g, yd.cpu().numpy()[:R]), "GroupGemm and DenseGemm bits differ"
+
+
+@pytest.mark.parametrize("name", ["ragged8", "fine"])
+def test_combine(name):
+    inp, ids, w = case(name)
+    s = inp.shape
+    g = Dev(inp)
+    counts, offsets, sorted_slot, slot_row = oracle.dispatch(ids, s.e0, s.EL)
+    R = int(offsets[-1])
+    rng = np.random.default_rng(3)
+    yp = rng.standard_normal((max(R, 1), s.H)).astype(np.float32)
+    init = rng.standard_normal((s.T, s.H)).astype(np.float32)
+    ref0 = oracle.combine(yp, slot_row.reshape(s.T, s.k), w)
+    ref1 = oracle.combine(yp, slot_row.reshape(s.T, s.k), w, init)
+    y = torch.full((s.T, s.H), float("nan"), dtype=torch.float32, device=dev())
+    moe.combine(g.d, 0, s.EL, f32(yp), i32(ids), i32(slot_row), f32(w), y, 0)
+    torch.cuda.synchronize()
+    assert_close(y.cpu().numpy(), ref0, "combine", max_abs=1e-5, rel_fro=1e-6)
+    # accumulate over stages in order: same bits as one call
+    y1 = f32(init)
+    moe.combine(g.d, 0, s.EL, f32(yp), i32(ids), i32(slot_row), f32(w), y1, 1)
+    y2 = f32(init)
+    half = s.EL // 2
+    moe.combine(g.d, 0, half, f32(yp), i32(ids), i32(slot_row), f32(w), y2, 1)
+    moe.combine(g.d, half, s.EL - half, f32(yp), i32(ids), i32(slot_row), f32(w), y2, 1)
+    torch.cuda.synchronize()
+    assert_close(y1.cpu().numpy(), ref1, "combine+init", max_abs=1e-5, rel_fro=1e-6)
+    assert torch.equal(y1, y2)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_forward(name):
+    inp, ids, w = case(name)
+    s = inp.shape
+    buf = Dev(inp).forward()
+    counts, *_ = oracle.dispatch(ids, s.e0, s.EL)
+    assert np.array_equal(buf.topk_ids.cpu().numpy(), ids)
+    assert weights_match(buf.topk_w.cpu().numpy(), w)
+    assert np.array_equal(buf.counts.cpu().numpy(), counts)
+    ref = oracle_y(inp, ids, w, np.arange(s.T))
+    assert_close(buf.y.cpu().numpy(), ref, f"{name} forward")
+
+
+@pytest.mark.parametrize("name", ["ragged8", "fine"])
+def test_forward_invariant_to_pipeline_and_gemm_kind(name):
+    """PN, the GEMM kind and a repeated call all give the same bits."""
+    inp, _, _ = case(name)
+    g = Dev(inp)
+    EL = inp.shape.EL
+    base = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP)).y.clone()
+    for pn in [p for p in (1, 2, 4, 5) if EL % p == 0]:
+        for mode in (moe.GEMM_GROUP, moe.GEMM_DENSE, moe.GEMM_AUTO):
+            y = g.forward(moe.opts(gemm_mode=mode, pipeline_n=pn)).y
+            assert torch.equal(y, base), f"PN={pn} mode={mode} differs"
+    y = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP, gemm_cu_budget=40)).y
+    assert torch.equal(y, base), "CU budget changes the bits"
+
+
+def test_forward_all_tokens_to_one_expert():
+    shp = C(name="hot", index=206, T=700, H=256, I=128, E=8, EL=8, k=1, renorm=True)
+    inp = synth.make_inputs(shp)
+    inp.bias = np.zeros(8, np.float32)
+    inp.bias[5] = 1e4
+    _, ids, w = oracle.route(inp.x, inp.w_router, inp.bias, 1, True)
+    assert np.all(ids == 5)
+    for mode in (moe.GEMM_GROUP, moe.GEMM_DENSE):
+        buf = Dev(inp).forward(moe.opts(gemm_mode=mode, pipeline_n=4))
+        assert np.array_equal(buf.counts.cpu().numpy(), [0, 0, 0, 0, 0, 700, 0, 0])
+        assert_close(buf.y.cpu().numpy(), oracle_y(inp, ids, w, np.arange(700)), "hot expert")
+
+
+def test_forward_no_local_rows():
+    """Every token routes outside the local window: y is exactly zero."""
+    shp = C(name="away", index=207, T=100, H=128, I=64, E=8, EL=2, e0=0, k=1, renorm=True)
+    inp = synth.make_inputs(shp)
+    inp.bias = np.zeros(8, np.float32)
+    inp.bias[6] = 1e4
+    buf = Dev(inp).forward(moe.opts(gemm_mode=moe.GEMM_AUTO, pipeline_n=2))
+    assert np.all(buf.counts.cpu().numpy() == 0)
+    assert torch.count_nonzero(buf.y).item() == 0
+
+
+def test_zero_tokens_is_a_noop():
+    shp = synth.SHAPES["tiny"]
+    d = moe.dims(0, shp.H, shp.I, shp.E, shp.k)
+    y = torch.full((1, shp.H), 3.0, device=dev())
+    ws = torch.empty(16, dtype=torch.uint8, device=dev())
+    dummy = torch.empty(1, dtype=torch.bfloat16, device=dev())
+    moe.forward(d, moe.opts(), dummy, f32(np.zeros(1)), None, dummy, dummy, dummy, None, None,
+                None, y, None, None, None, ws)
+    torch.cuda.synchronize()
+    assert torch.all(y == 3.0)

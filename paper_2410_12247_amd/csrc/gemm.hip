@@ -109,7 +109,9 @@ __device__ __forceinline__ void run_tile(const TileArgs &a, bf16_t *smem) {
     using C = Cfg<MODE, BN, BM, BK, NS>;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    // wave index as a scalar: everything derived from it (LDS-DMA targets,
+    // which weight half a wave copies) stays in SGPRs
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wn = wave % C::WN;
     const int wm = wave / C::WN;
     const int K = a.K;
@@ -136,31 +138,36 @@ __device__ __forceinline__ void run_tile(const TileArgs &a, bf16_t *smem) {
         wsrc = a.w0;
         wrow0 = wave * (BN / 4);
     }
-    int woff[C::W_INSTR];
+    // per-lane byte offsets from the (scalar) tile base; rows past the valid
+    // range read a valid row, whose results are never stored
+    uint32_t woff[C::W_INSTR];
 #pragma unroll
     for (int i = 0; i < C::W_INSTR; ++i) {
-        const int r = min(wrow0 + i * C::RPI + drow, a.n_valid - 1);  // tails read a valid row
-        woff[i] = r * K + dchunk;
+        const int r = min(wrow0 + i * C::RPI + drow, a.n_valid - 1);
+        woff[i] = (uint32_t)(r * K + dchunk) * 2u;
     }
-    int xoff[C::X_INSTR];
+    uint32_t xoff[C::X_INSTR];
 #pragma unroll
     for (int i = 0; i < C::X_INSTR; ++i) {
         const int r = min(wave * (BM / 4) + i * C::RPI + drow, a.m_valid - 1);
-        xoff[i] = r * K + dchunk;
+        xoff[i] = (uint32_t)(r * K + dchunk) * 2u;
     }
     const int w_lds = wave * (BN / 4) * BK;  // element offset of this wave's rows
     const int x_lds = C::STAGE_W + wave * (BM / 4) * BK;
 
+    // scalar base + per-lane 32-bit offset: the SADDR form of the load
     auto issue = [&](int stage, int k0) {
         bf16_t *sb = smem + stage * C::STAGE;
+        const char *wk = reinterpret_cast<const char *>(wsrc + k0);
+        const char *xk = reinterpret_cast<const char *>(a.x + k0);
 #pragma unroll
         for (int i = 0; i < C::W_INSTR; ++i)
-            __builtin_amdgcn_global_load_lds((gbl_void_t *)(wsrc + woff[i] + k0),
+            __builtin_amdgcn_global_load_lds((gbl_void_t *)(wk + woff[i]),
                                              (lds_void_t *)(sb + w_lds + i * C::RPI * BK), 16,
                                              0, 0);
 #pragma unroll
         for (int i = 0; i < C::X_INSTR; ++i)
-            __builtin_amdgcn_global_load_lds((gbl_void_t *)(a.x + xoff[i] + k0),
+            __builtin_amdgcn_global_load_lds((gbl_void_t *)(xk + xoff[i]),
                                              (lds_void_t *)(sb + x_lds + i * C::RPI * BK), 16,
                                              0, 0);
     };
@@ -180,51 +187,285 @@ __device__ __forceinline__ void run_tile(const TileArgs &a, bf16_t *smem) {
     const int lk = lane >> 4;  // which 8-wide k group of the 32-wide MFMA step
     const int lsw = swz<BK>(lrow);
 
-    auto compute = [&](int stage) {
+    // Operand fragments are double-buffered in registers: while the MFMAs
+    // of stage kt run, the fragments of stage kt+1 are read from LDS.
+    struct Frags {
+        bf16x8 a[C::TN];
+        bf16x8 b[C::TM];
+    };
+    static_assert(BK == 32, "one 32-wide MFMA step per stage");
+    static_assert(NS == 4, "the K loop below is unrolled for four stages");
+    Frags f0, f1;
+
+    auto load_frags = [&](int stage, Frags &f) {
         const bf16_t *sw = smem + stage * C::STAGE;
         const bf16_t *sx = sw + C::STAGE_W;
+        const int chunk = (lk ^ lsw) * 8;
 #pragma unroll
-        for (int s = 0; s < BK / 32; ++s) {
-            const int chunk = ((s * 4 + lk) ^ lsw) * 8;
-            bf16x8 af[C::TN], bfr[C::TM];
+        for (int t = 0; t < C::TN; ++t)
+            f.a[t] = *reinterpret_cast<const bf16x8 *>(sw + (arow[t] + lrow) * BK + chunk);
+#pragma unroll
+        for (int m = 0; m < C::TM; ++m)
+            f.b[m] = *reinterpret_cast<const bf16x8 *>(
+                sx + (wm * C::WTM + m * 16 + lrow) * BK + chunk);
+    };
+    auto mfmas = [&](const Frags &f) {
+#pragma unroll
+        for (int m = 0; m < C::TM; ++m)
 #pragma unroll
             for (int t = 0; t < C::TN; ++t)
-                af[t] = *reinterpret_cast<const bf16x8 *>(sw + (arow[t] + lrow) * BK + chunk);
+                acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[t], f.b[m], acc[t][m],
+                                                                    0, 0, 0);
+    };
+    // one LDS read issued between every (TN*TM)/(TN+TM) MFMAs
+    auto interleave = [&]() {
+        constexpr int NREAD = C::TN + C::TM;
+        constexpr int PER = (C::TN * C::TM) / NREAD;
 #pragma unroll
-            for (int m = 0; m < C::TM; ++m)
-                bfr[m] = *reinterpret_cast<const bf16x8 *>(
-                    sx + (wm * C::WTM + m * 16 + lrow) * BK + chunk);
-#pragma unroll
-            for (int m = 0; m < C::TM; ++m)
-#pragma unroll
-                for (int t = 0; t < C::TN; ++t)
-                    acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[t], bfr[m],
-                                                                        acc[t][m], 0, 0, 0);
+        for (int i = 0; i < NREAD; ++i) {
+            if (i < C::LPS) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                  // DS read
+            __builtin_amdgcn_sched_group_barrier(0x008, PER, 0);                // MFMA
+        }
+    };
+    // stage kt lives in LDS buffer u = kt % NS and in register set cur
+    auto step = [&](int kt, int u, Frags &cur, Frags &nxt) {
+        const bool ahead = kt + NS - 1 < nk;
+        // Stage kt+NS-1 is requested unconditionally (past the end it re-reads
+        // the last stage into a buffer that is never read again), so the
+        // loads, LDS reads and MFMAs form one block the scheduler interleaves.
+        issue((u + NS - 1) % NS, (ahead ? kt + NS - 1 : nk - 1) * BK);
+        // the prefetch of stage kt+1 is unconditional: past the last stage it
+        // reads a stale (in-bounds) LDS buffer whose values are never used,
+        // which keeps a single MFMA block (accumulators stay in AGPRs)
+        load_frags((u + 1) % NS, nxt);
+        mfmas(cur);
+        interleave();
+        if (kt + 2 < nk) {
+            // stage kt+2 must be in LDS (every wave's share) before the next
+            // step reads it
+            if (ahead) wait_vmcnt<(NS - 3) * C::LPS>(); else wait_vmcnt<0>();
+            __builtin_amdgcn_s_barrier();
         }
     };
 
+    // prologue: stages 0..NS-2 requested; stage 0 in registers, stage 1 in LDS
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
         if (s < nk) issue(s, s * BK);
     if (nk >= NS - 1) wait_vmcnt<(NS - 2) * C::LPS>(); else wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
+    load_frags(0, f0);
+    if (nk >= NS - 1) wait_vmcnt<(NS - 3) * C::LPS>(); else wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
 
     for (int kt0 = 0; kt0 < nk; kt0 += NS) {
+        step(kt0, 0, f0, f1);
+        if (kt0 + 1 < nk) step(kt0 + 1, 1, f1, f0);
+        if (kt0 + 2 < nk) step(kt0 + 2, 2, f0, f1);
+        if (kt0 + 3 < nk) step(kt0 + 3, 3, f1, f0);
+    }
+    __builtin_amdgcn_s_barrier();  // LDS free for the next tile of this workgroup
+
+    // ---- epilogue: lane holds output columns col..col+3 of token row `row`
+    const int lcol4 = (lane >> 4) * 4;
+    if (MODE == 0) {
+        bf16_t *out = reinterpret_cast<bf16_t *>(a.out);
 #pragma unroll
-        for (int u = 0; u < NS; ++u) {
-            const int kt = kt0 + u;
-            if (kt < nk) {
-                const bool ahead = kt + NS - 1 < nk;
-                if (ahead) issue((u + NS - 1) % NS, (kt + NS - 1) * BK);
-                compute(u);
-                if (kt + 1 < nk) {
-                    if (ahead) wait_vmcnt<(NS - 2) * C::LPS>(); else wait_vmcnt<0>();
-                    __builtin_amdgcn_s_barrier();
+        for (int t = 0; t < C::TN / 2; ++t) {
+            const int col = wn * (C::WTN / 2) + t * 16 + lcol4;
+#pragma unroll
+            for (int m = 0; m < C::TM; ++m) {
+                const int row = wm * C::WTM + m * 16 + lrow;
+                if (row < a.m_valid && col < a.n_valid) {
+                    const floatx4 g = acc[t][m];
+                    const floatx4 u = acc[t + C::TN / 2][m];
+                    uint2 v;
+                    v.x = pack_bf16x2(silu_mul(g[0], u[0]), silu_mul(g[1], u[1]));
+                    v.y = pack_bf16x2(silu_mul(g[2], u[2]), silu_mul(g[3], u[3]));
+                    *reinterpret_cast<uint2 *>(out + row * a.ldo + col) = v;
                 }
             }
         }
+    } else {
+        float *out = reinterpret_cast<float *>(a.out);
+#pragma unroll
+        for (int t = 0; t < C::TN; ++t) {
+            const int col = wn * C::WTN + t * 16 + lcol4;
+#pragma unroll
+            for (int m = 0; m < C::TM; ++m) {
+                const int row = wm * C::WTM + m * 16 + lrow;
+                if (row < a.m_valid && col < a.n_valid)
+                    *reinterpret_cast<floatx4 *>(out + row * a.ldo + col) = acc[t][m];
+            }
+        }
     }
-    __builtin_amdgcn_s_barrier();  // LDS free for the next tile of this workgroup
+}
+
+// ---------------------------------------------------------------------------
+// Eight-wave ping-pong variant.  256 x 256 output tile, eight waves in two
+// groups of four, one wave of each group on every SIMD.  Each wave owns a
+// 128 (weights) x 64 (tokens) accumulator block (128 AGPRs).  The groups
+// alternate between a compute phase (32 MFMAs on fragments already in
+// registers) and a memory phase (its share of the LDS-DMA for stage k+3 and
+// the 12 fragment reads of its next stage), separated by workgroup
+// barriers, so every SIMD always has one wave issuing MFMAs while the other
+// feeds LDS.  Stage s lives in LDS buffer s % 4.
+//   group A (waves 0-3, token rows   0..127): compute(k) | mem: frags(k+1), DMA(k+3)
+//   group B (waves 4-7, token rows 128..255): mem: frags(k), DMA(k+3) | compute(k)
+// ---------------------------------------------------------------------------
+constexpr int PP_THREADS = 512;
+
+template <int MODE>
+struct PPCfg {
+    static constexpr int BN = 256, BM = 256, BK = 32, NS = 4;
+    static constexpr int WTN = 128, WTM = 64;  // wave tile (weights x tokens)
+    static constexpr int TN = WTN / 16, TM = WTM / 16;
+    static constexpr int CPR = BK / 8;          // 16-byte chunks per LDS row
+    static constexpr int RPI = 64 / CPR;        // rows one LDS-DMA instruction fills
+    static constexpr int W_INSTR = BN / 8 / RPI;
+    static constexpr int X_INSTR = BM / 8 / RPI;
+    static constexpr int LPS = W_INSTR + X_INSTR;  // DMA instructions per wave per stage
+    static constexpr int STAGE_W = BN * BK, STAGE_X = BM * BK, STAGE = STAGE_W + STAGE_X;
+    static constexpr int LDS_ELEMS = NS * STAGE;
+    static constexpr int BNOUT = MODE == 0 ? BN / 2 : BN;
+};
+
+template <int MODE>
+__device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
+    using C = PPCfg<MODE>;
+    constexpr int BK = C::BK, NS = C::NS;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int grp = wave >> 2;  // 0 = A, 1 = B
+    const int wn = wave & 1;    // weight half
+    const int wm = wave >> 1;   // 64-row token block
+    const int K = a.K;
+    const int nk = K / BK;
+
+    floatx4 acc[C::TN][C::TM];
+#pragma unroll
+    for (int t = 0; t < C::TN; ++t)
+#pragma unroll
+        for (int m = 0; m < C::TM; ++m) acc[t][m] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // ---- LDS-DMA share of this wave: 32 weight rows and 32 token rows
+    const int drow = lane / C::CPR;
+    const int dchunk = ((lane % C::CPR) ^ swz<BK>(drow)) * 8;
+    const bf16_t *wsrc;
+    int wrow0;
+    if (MODE == 0) {  // waves 0..3 copy gate rows, 4..7 up rows
+        wsrc = wave >= 4 ? a.w1 : a.w0;
+        wrow0 = (wave & 3) * (C::BN / 8);
+    } else {
+        wsrc = a.w0;
+        wrow0 = wave * (C::BN / 8);
+    }
+    uint32_t woff[C::W_INSTR], xoff[C::X_INSTR];
+#pragma unroll
+    for (int i = 0; i < C::W_INSTR; ++i) {
+        const int r = min(wrow0 + i * C::RPI + drow, a.n_valid - 1);
+        woff[i] = (uint32_t)(r * K + dchunk) * 2u;
+    }
+#pragma unroll
+    for (int i = 0; i < C::X_INSTR; ++i) {
+        const int r = min(wave * (C::BM / 8) + i * C::RPI + drow, a.m_valid - 1);
+        xoff[i] = (uint32_t)(r * K + dchunk) * 2u;
+    }
+    const int w_lds = wave * (C::BN / 8) * BK;
+    const int x_lds = C::STAGE_W + wave * (C::BM / 8) * BK;
+    auto issue = [&](int kstage) {  // this wave's share of stage kstage (clamped)
+        const int ks = min(kstage, nk - 1);
+        bf16_t *sb = smem + (kstage % NS) * C::STAGE;
+        const char *wk = reinterpret_cast<const char *>(wsrc + ks * BK);
+        const char *xk = reinterpret_cast<const char *>(a.x + ks * BK);
+#pragma unroll
+        for (int i = 0; i < C::W_INSTR; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void_t *)(wk + woff[i]),
+                                             (lds_void_t *)(sb + w_lds + i * C::RPI * BK), 16,
+                                             0, 0);
+#pragma unroll
+        for (int i = 0; i < C::X_INSTR; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void_t *)(xk + xoff[i]),
+                                             (lds_void_t *)(sb + x_lds + i * C::RPI * BK), 16,
+                                             0, 0);
+    };
+
+    // ---- fragments of this wave
+    int arow[C::TN];
+#pragma unroll
+    for (int t = 0; t < C::TN; ++t) {
+        if (MODE == 0)
+            arow[t] = t < C::TN / 2 ? wn * (C::WTN / 2) + t * 16
+                                    : C::BN / 2 + wn * (C::WTN / 2) + (t - C::TN / 2) * 16;
+        else
+            arow[t] = wn * C::WTN + t * 16;
+    }
+    const int lrow = lane & 15;
+    const int chunk = ((lane >> 4) ^ swz<BK>(lrow)) * 8;
+    bf16x8 fa[C::TN], fb[C::TM];
+    auto load_frags = [&](int kstage) {  // stale but in-bounds past the end
+        const bf16_t *sw = smem + (kstage % NS) * C::STAGE;
+        const bf16_t *sx = sw + C::STAGE_W;
+#pragma unroll
+        for (int t = 0; t < C::TN; ++t)
+            fa[t] = *reinterpret_cast<const bf16x8 *>(sw + (arow[t] + lrow) * BK + chunk);
+#pragma unroll
+        for (int m = 0; m < C::TM; ++m)
+            fb[m] = *reinterpret_cast<const bf16x8 *>(sx + (wm * C::WTM + m * 16 + lrow) * BK +
+                                                      chunk);
+    };
+    auto mfmas = [&]() {
+#pragma unroll
+        for (int m = 0; m < C::TM; ++m)
+#pragma unroll
+            for (int t = 0; t < C::TN; ++t)
+                acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[t], fb[m], acc[t][m], 0,
+                                                                    0, 0);
+    };
+
+    // prologue: stages 0..2 requested by every wave, all landed
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) issue(s);
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+
+    if (grp == 0) {
+        load_frags(0);
+        for (int k = 0; k < nk; ++k) {
+            // compute phase: stage k
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            __builtin_amdgcn_s_setprio(1);
+            mfmas();
+            __builtin_amdgcn_s_setprio(0);
+            // stage k+1 (requested two iterations ago) landed before the barrier
+            wait_vmcnt<C::LPS>();
+            __builtin_amdgcn_s_barrier();
+            // memory phase: fragments of stage k+1, this wave's share of stage k+3
+            load_frags(k + 1);
+            issue(k + NS - 1);
+            __builtin_amdgcn_s_barrier();
+        }
+    } else {
+        for (int k = 0; k < nk; ++k) {
+            // memory phase: fragments of stage k, this wave's share of stage k+3
+            load_frags(k);
+            issue(k + NS - 1);
+            // stage k+1 (requested in iteration k-2) landed; the requests of
+            // iterations k-1 and k may stay in flight
+            wait_vmcnt<2 * C::LPS>();
+            __builtin_amdgcn_s_barrier();
+            // compute phase: stage k
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            __builtin_amdgcn_s_setprio(1);
+            mfmas();
+            __builtin_amdgcn_s_setprio(0);
+            __builtin_amdgcn_s_barrier();
+        }
+    }
+    wait_vmcnt<0>();  // clamped tail requests drained before LDS is reused
+    __builtin_amdgcn_s_barrier();
 
     // ---- epilogue: lane holds output columns col..col+3 of token row `row`
     const int lcol4 = (lane >> 4) * 4;
@@ -272,21 +513,45 @@ __device__ __forceinline__ void decode_tile(int tau, int MT, int NT, int &mt, in
     nt = sc * GROUP_N + (r - mt * width);
 }
 
-template <int MODE, int BN, int BM, int BK, int NS>
-__global__ __launch_bounds__(NTHREADS, 1) void dense_kernel(const bf16_t *__restrict__ x,
+// Tile policies shared by the two schedulers.
+template <int MODE, int BN_, int BM_, int BK, int NS>
+struct FourWave {
+    using C = Cfg<MODE, BN_, BM_, BK, NS>;
+    static constexpr int THREADS = NTHREADS;
+    static constexpr int BM = BM_;
+    static constexpr int BNOUT = C::BNOUT;
+    static constexpr int LDS_ELEMS = NS * C::STAGE;
+    static __device__ __forceinline__ void run(const TileArgs &a, bf16_t *smem) {
+        run_tile<MODE, BN_, BM_, BK, NS>(a, smem);
+    }
+};
+template <int MODE>
+struct PingPong {
+    using C = PPCfg<MODE>;
+    static constexpr int THREADS = PP_THREADS;
+    static constexpr int BM = C::BM;
+    static constexpr int BNOUT = C::BNOUT;
+    static constexpr int LDS_ELEMS = C::LDS_ELEMS;
+    static __device__ __forceinline__ void run(const TileArgs &a, bf16_t *smem) {
+        run_tile_pp<MODE>(a, smem);
+    }
+};
+
+template <int MODE, class TP>
+__global__ __launch_bounds__(TP::THREADS) void dense_kernel(const bf16_t *__restrict__ x,
                                                             int64_t rows, const bf16_t *w0,
                                                             const bf16_t *w1, int N, int K,
                                                             void *out, int64_t ldo, int MT,
                                                             int NT) {
-    using C = Cfg<MODE, BN, BM, BK, NS>;
-    __shared__ __attribute__((aligned(16))) bf16_t smem[NS * C::STAGE];
+    constexpr int BM = TP::BM;
+    __shared__ __attribute__((aligned(16))) bf16_t smem[TP::LDS_ELEMS];
     const int per = gridDim.x / NXCD;
     const int tau = (blockIdx.x % NXCD) * per + blockIdx.x / NXCD;
     if (tau >= MT * NT) return;
     int mt, nt;
     decode_tile(tau, MT, NT, mt, nt);
     TileArgs a;
-    const int64_t n0 = (int64_t)nt * C::BNOUT;
+    const int64_t n0 = (int64_t)nt * TP::BNOUT;
     const int64_t m0 = (int64_t)mt * BM;
     a.w0 = w0 + n0 * K;
     a.w1 = MODE == 0 ? w1 + n0 * K : nullptr;
@@ -299,22 +564,22 @@ __global__ __launch_bounds__(NTHREADS, 1) void dense_kernel(const bf16_t *__rest
         a.out = reinterpret_cast<bf16_t *>(out) + m0 * ldo + n0;
     else
         a.out = reinterpret_cast<float *>(out) + m0 * ldo + n0;
-    run_tile<MODE, BN, BM, BK, NS>(a, smem);
+    TP::run(a, smem);
 }
 
-template <int MODE, int BN, int BM, int BK, int NS>
-__global__ __launch_bounds__(NTHREADS, 1) void group_kernel(
+template <int MODE, class TP>
+__global__ __launch_bounds__(TP::THREADS) void group_kernel(
     const int32_t *__restrict__ offsets, int e_first, int e_count, const bf16_t *__restrict__ x,
     const bf16_t *w0s, const bf16_t *w1s, int64_t wstride, int N, int K, void *out,
     int64_t ldo) {
-    using C = Cfg<MODE, BN, BM, BK, NS>;
-    __shared__ __attribute__((aligned(16))) bf16_t smem[NS * C::STAGE];
+    constexpr int BM = TP::BM;
+    __shared__ __attribute__((aligned(16))) bf16_t smem[TP::LDS_ELEMS];
     __shared__ int s_off[kMaxExperts + 1];
     __shared__ int s_pre[kMaxExperts + 1];
     const int tid = threadIdx.x;
-    const int NT = (N + C::BNOUT - 1) / C::BNOUT;
+    const int NT = (N + TP::BNOUT - 1) / TP::BNOUT;
 
-    for (int i = tid; i <= e_count; i += NTHREADS) s_off[i] = offsets[e_first + i];
+    for (int i = tid; i <= e_count; i += TP::THREADS) s_off[i] = offsets[e_first + i];
     __syncthreads();
     // tiles per expert, then an inclusive scan (Hillis-Steele over <= 256)
     int mine = 0;
@@ -345,7 +610,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void group_kernel(
         const int MT = (cnt + BM - 1) / BM;
         int mt, nt;
         decode_tile(tau - s_pre[e], MT, NT, mt, nt);
-        const int64_t n0 = (int64_t)nt * C::BNOUT;
+        const int64_t n0 = (int64_t)nt * TP::BNOUT;
         const int64_t r0 = (int64_t)s_off[e] + (int64_t)mt * BM;
         TileArgs a;
         const int64_t woffe = (int64_t)(e_first + e) * wstride;
@@ -360,15 +625,21 @@ __global__ __launch_bounds__(NTHREADS, 1) void group_kernel(
             a.out = reinterpret_cast<bf16_t *>(out) + r0 * ldo + n0;
         else
             a.out = reinterpret_cast<float *>(out) + r0 * ldo + n0;
-        run_tile<MODE, BN, BM, BK, NS>(a, smem);
+        TP::run(a, smem);
     }
 }
 
-// Tile shapes: BN weight rows x BM token rows, BK k per stage, NS stages.
-constexpr int DENSE_BN = 256, DENSE_BM = 256, DENSE_BK = 32, DENSE_NS = 4;
-constexpr int GROUP_BN = 256, GROUP_BM = 256, GROUP_BK = 32, GROUP_NS = 4;
-#define DENSE_CFG DENSE_BN, DENSE_BM, DENSE_BK, DENSE_NS
-#define GROUP_CFG GROUP_BN, GROUP_BM, GROUP_BK, GROUP_NS
+// Tile policy of each scheduler.
+#ifndef MOE_GEMM_PINGPONG
+#define MOE_GEMM_PINGPONG 1
+#endif
+#if MOE_GEMM_PINGPONG
+template <int MODE> using DenseTile = PingPong<MODE>;
+template <int MODE> using GroupTile = PingPong<MODE>;
+#else
+template <int MODE> using DenseTile = FourWave<MODE, 256, 256, 32, 4>;
+template <int MODE> using GroupTile = FourWave<MODE, 256, 256, 32, 4>;
+#endif
 
 int round_grid(int64_t tiles) { return (int)(((tiles + NXCD - 1) / NXCD) * NXCD); }
 
@@ -377,10 +648,10 @@ int round_grid(int64_t tiles) { return (int)(((tiles + NXCD - 1) / NXCD) * NXCD)
 hipError_t launch_dense_gateup(int64_t rows, int H, int I, const bf16_t *x, const bf16_t *w_gate,
                                const bf16_t *w_up, bf16_t *act, hipStream_t s) {
     if (rows <= 0) return hipSuccess;
-    using C = Cfg<0, DENSE_CFG>;
-    const int MT = (int)((rows + DENSE_BM - 1) / DENSE_BM);
-    const int NT = (I + C::BNOUT - 1) / C::BNOUT;
-    dense_kernel<0, DENSE_CFG><<<round_grid((int64_t)MT * NT), NTHREADS, 0, s>>>(
+    using TP = DenseTile<0>;
+    const int MT = (int)((rows + TP::BM - 1) / TP::BM);
+    const int NT = (I + TP::BNOUT - 1) / TP::BNOUT;
+    dense_kernel<0, TP><<<round_grid((int64_t)MT * NT), TP::THREADS, 0, s>>>(
         x, rows, w_gate, w_up, I, H, act, I, MT, NT);
     return hipGetLastError();
 }
@@ -388,10 +659,10 @@ hipError_t launch_dense_gateup(int64_t rows, int H, int I, const bf16_t *x, cons
 hipError_t launch_dense_down(int64_t rows, int H, int I, const bf16_t *act,
                              const bf16_t *w_down, float *y, hipStream_t s) {
     if (rows <= 0) return hipSuccess;
-    using C = Cfg<1, DENSE_CFG>;
-    const int MT = (int)((rows + DENSE_BM - 1) / DENSE_BM);
-    const int NT = (H + C::BNOUT - 1) / C::BNOUT;
-    dense_kernel<1, DENSE_CFG><<<round_grid((int64_t)MT * NT), NTHREADS, 0, s>>>(
+    using TP = DenseTile<1>;
+    const int MT = (int)((rows + TP::BM - 1) / TP::BM);
+    const int NT = (H + TP::BNOUT - 1) / TP::BNOUT;
+    dense_kernel<1, TP><<<round_grid((int64_t)MT * NT), TP::THREADS, 0, s>>>(
         act, rows, w_down, nullptr, H, I, y, H, MT, NT);
     return hipGetLastError();
 }
@@ -401,9 +672,10 @@ hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
                                const bf16_t *w_gate, const bf16_t *w_up, bf16_t *act,
                                int grid, hipStream_t s) {
     if (e_count <= 0) return hipSuccess;
-    group_kernel<0, GROUP_CFG><<<grid, NTHREADS, 0, s>>>(
-        offsets, e_first, e_count, x_perm, w_gate, w_up, (int64_t)d.inter * d.hidden, d.inter,
-        d.hidden, act, d.inter);
+    using TP = GroupTile<0>;
+    group_kernel<0, TP><<<grid, TP::THREADS, 0, s>>>(offsets, e_first, e_count, x_perm, w_gate,
+                                                     w_up, (int64_t)d.inter * d.hidden, d.inter,
+                                                     d.hidden, act, d.inter);
     return hipGetLastError();
 }
 
@@ -411,9 +683,10 @@ hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
                              const int32_t *offsets, const bf16_t *act,
                              const bf16_t *w_down, float *y_perm, int grid, hipStream_t s) {
     if (e_count <= 0) return hipSuccess;
-    group_kernel<1, GROUP_CFG><<<grid, NTHREADS, 0, s>>>(
-        offsets, e_first, e_count, act, w_down, nullptr, (int64_t)d.hidden * d.inter, d.hidden,
-        d.inter, y_perm, d.hidden);
+    using TP = GroupTile<1>;
+    group_kernel<1, TP><<<grid, TP::THREADS, 0, s>>>(offsets, e_first, e_count, act, w_down,
+                                                     nullptr, (int64_t)d.hidden * d.inter,
+                                                     d.hidden, d.inter, y_perm, d.hidden);
     return hipGetLastError();
 }
 

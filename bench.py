@@ -145,6 +145,25 @@ def run_workload(args, shape, inp, steps, warmup, timing=True):
     return wall, tms, counts
 
 
+def measured_traffic(workload, kernel_prefix):
+    """HBM bytes per launch of a GEMM kernel from the committed rocprofv3
+    counter summary (FETCH_SIZE / WRITE_SIZE scaled by the copy calibration),
+    or None when the GEMM source changed since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_counters.json")
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    src = open(os.path.join(ROOT, "paper_2410_12247_amd", "csrc", "gemm.hip"), "rb").read()
+    if d.get("gemm_source_sha256") != hashlib.sha256(src).hexdigest():
+        return None
+    for k, v in d["kernels"].items():
+        if k.startswith(kernel_prefix):
+            return v["bytes"]
+    return None
+
+
 def summarize_timing(tms):
     keys = tms[0].keys()
     return {k: sum(t[k] for t in tms) / len(tms) for k in keys}
@@ -185,6 +204,11 @@ def main(argv=None):
     per_launch_flops = fg / max(tm["gateup_launches"], 1)
     achieved = per_launch_flops / (per_launch_ms * 1e-3) / 1e12
     peak = PEAK_BF16_FLOPS / 1e12
+    traffic = None
+    if tm["group_stages"] and not tm["dense_stages"] and args.pn == 1 and not args.tokens:
+        kname = "group_kernel<0"
+        t = measured_traffic(f"{args.config}_group", kname)
+        traffic = None if t is None else round(t)
     line = {
         "metric": METRIC,
         "value": round(shape.T / (ms * 1e-3), 1),
@@ -206,7 +230,8 @@ def main(argv=None):
                    "gemm_mode": args.mode, "pipeline_n": args.pn,
                    "gemm_cu_budget": args.cu_budget, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "traffic": traffic,
                      "kernel": "gate/up GEMM (fused SiLU*mul)",
                      "per_launch_ms": round(per_launch_ms, 4),
                      "per_launch_gflop": round(per_launch_flops / 1e9, 2)},

@@ -72,8 +72,9 @@ enum { MOE_FLAG_TIMING = 1 };
 typedef struct {
     int32_t gemm_mode;      /* MOE_GEMM_AUTO, _GROUP or _DENSE */
     int32_t dense_min_rows; /* AUTO picks DenseGemm for a pipeline stage when
-                               its experts average at least this many rows;
-                               0 = built-in default measured on MI355X */
+                               every expert in it has at least this many
+                               rows, else GroupGemm; 0 = built-in default
+                               (see moe_default_dense_min_rows) */
     int32_t pipeline_n;     /* PN >= 1, must divide local_count: stage s owns
                                local experts [s*EL/PN, (s+1)*EL/PN) */
     int32_t gemm_cu_budget; /* workgroups of the persistent grouped GEMM;
@@ -192,7 +193,8 @@ moe_status moe_combine(const moe_dims *dims, int32_t e_first, int32_t e_count,
  * ws: at least moe_workspace_bytes(dims, opts) bytes of device memory.
  * Ordered after prior work on `stream` and finished on `stream`.  When the
  * policy needs row counts on the host (gemm_mode != GROUP or PN > 1) the
- * call blocks the host once on a 4*EL-byte device-to-host copy. */
+ * call blocks the host once on a 4*EL-byte device-to-host copy (AUTO needs
+ * the counts only when its threshold can be reached by some expert). */
 moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe_bf16 *x,
                            const float *w_router, const float *bias,
                            const moe_bf16 *w_gate, const moe_bf16 *w_up,
@@ -206,7 +208,8 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
 moe_status moe_last_timing(moe_timing *out);
 
 /* The dense-GEMM threshold (rows per expert) AUTO uses when
- * dense_min_rows == 0. */
+ * dense_min_rows == 0.  On MI355X the grouped GEMM won at every measured
+ * load, so the built-in value (2^30) is never reached. */
 int32_t moe_default_dense_min_rows(void);
 
 const char *moe_status_string(moe_status s);

@@ -23,7 +23,13 @@
 namespace moe {
 namespace {
 
-constexpr int32_t kDefaultDenseMinRows = 4096;
+// AUTO's DenseGemm threshold (rows of every expert of a stage).  Measured on
+// MI355X over the skewed DeepSeekV2-shaped sweep (T = 64 .. 65536, up to
+// 58K rows on one expert) and the Mixtral / DBRX shards, the grouped launch
+// beat per-expert dense launches at every load (one tile wave tail instead
+// of one per expert, same MFMA tile), so the built-in threshold is never
+// reached; callers can lower it through moe_opts.dense_min_rows.
+constexpr int32_t kDefaultDenseMinRows = 1 << 30;
 
 enum Phase {
     PH_ROUTE, PH_PERMUTE, PH_GATHER, PH_GATEUP, PH_DOWN, PH_SHARED, PH_COMBINE, PH_TOTAL, PH_N
@@ -218,7 +224,13 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
 
     // GEMM kind per stage needs the row counts on the host
     std::vector<int32_t> hc;
-    const bool need_counts = o->gemm_mode != MOE_GEMM_GROUP || PN > 1;
+    const int32_t m_star = o->dense_min_rows > 0 ? o->dense_min_rows : kDefaultDenseMinRows;
+    // row counts are needed on the host to size per-expert dense launches and
+    // stage gathers; AUTO is GROUP without a sync when no expert can reach the
+    // threshold (an expert has at most T rows) and PN = 1
+    const bool need_counts =
+        o->gemm_mode == MOE_GEMM_DENSE || PN > 1 ||
+        (o->gemm_mode == MOE_GEMM_AUTO && m_star <= d.tokens);
     if (need_counts) {
         MOE_HIP(hipMemcpyAsync(st->pinned_counts, cnt, sizeof(int32_t) * EL,
                                hipMemcpyDeviceToHost, s0));
@@ -226,7 +238,6 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
         MOE_HIP(hipEventSynchronize(ev_counts));
         hc.assign(st->pinned_counts, st->pinned_counts + EL);
     }
-    const int32_t m_star = o->dense_min_rows > 0 ? o->dense_min_rows : kDefaultDenseMinRows;
     int grid = o->gemm_cu_budget > 0 ? o->gemm_cu_budget : device_cu_count();
     grid = std::max(8, (grid / 8) * 8);
 
@@ -241,9 +252,12 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
         bool dense = o->gemm_mode == MOE_GEMM_DENSE;
         if (need_counts) {
             stage_rows = 0;
-            for (int e = ef; e < ef + per_stage; ++e) stage_rows += hc[e];
-            if (o->gemm_mode == MOE_GEMM_AUTO)
-                dense = stage_rows >= (int64_t)m_star * per_stage;
+            int32_t min_rows = INT32_MAX;
+            for (int e = ef; e < ef + per_stage; ++e) {
+                stage_rows += hc[e];
+                min_rows = std::min(min_rows, hc[e]);
+            }
+            if (o->gemm_mode == MOE_GEMM_AUTO) dense = min_rows >= m_star;
         }
         // gather (dispatch of this expert group)
         MOE_TRY(tm.begin(st->sg, PH_GATHER));

@@ -1,10 +1,10 @@
 // Router: fp32 logits, top-k selection and softmax weights in one kernel.
 //
-// Logits (the topKGating operator): each lane owns one token and a wave owns
-// a quarter of the experts, so every logit is ONE fp32 fma chain over h in
-// ascending order, started from +0, with the bias added once at the end --
-// the same bits as a sequential fma loop on the CPU.  x and the router are
-// staged through LDS 32 h at a time; router reads are wave-wide broadcasts.
+// Logits (the topKGating operator): every logit is ONE fp32 fma chain over
+// h in ascending order, started from +0, with the bias added once at the
+// end -- the same bits as a sequential fma loop on the CPU.  A thread keeps
+// a 4-token x TE-expert block of chains in registers; x and the router are
+// staged through LDS 32 h at a time.
 //
 // Selection: the token's logits are spread over a wave (lane l holds experts
 // l, l+64, l+128, l+192); each of the k rounds is a wave-wide max of 64-bit
@@ -17,7 +17,7 @@
 namespace moe {
 namespace {
 
-constexpr int RT_TOK = 64;  // tokens per workgroup (one per lane)
+constexpr int RT_TOK = 64;  // tokens per workgroup
 constexpr int RT_HC = 32;   // h per LDS chunk
 constexpr int RT_LD = RT_HC + 4;
 constexpr int RT_THREADS = 256;
@@ -94,85 +94,131 @@ __device__ __forceinline__ float key_logit(uint64_t key) {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// RE: maximum experts per wave (E <= 4*RE).
-template <int RE>
+// Logits phase layout: 256 threads = 16 token groups x 16 expert groups;
+// a thread owns TT = 4 tokens x TE experts (TE = ceil(E / 16)) and keeps
+// their fma chains in registers.  x and the router are staged through LDS
+// RT_HC h at a time (the next chunk is fetched into registers while the
+// current one is multiplied); per 4 h a thread reads TT + TE float4 and
+// issues 4*TT*TE fmas.
+constexpr int RT_TT = 4;   // tokens per thread
+constexpr int RT_TG = 16;  // token groups
+constexpr int RT_EG = 16;  // expert groups
+static_assert(RT_TT * RT_TG == RT_TOK, "token tiling");
+
+template <int TE>
 __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restrict__ x,
                                                            const float *__restrict__ wr,
                                                            const float *__restrict__ bias,
                                                            int64_t T, int H, int E, int k,
                                                            int renorm, int32_t *__restrict__ ids,
                                                            float *__restrict__ wout) {
-    constexpr int EMAX = 4 * RE;
-    constexpr int P1 = RT_TOK * RT_LD + EMAX * RT_LD;  // floats, logits phase
+    constexpr int EMAX = RT_EG * TE;
+    constexpr int P1 = RT_TOK * RT_LD + (EMAX + 1) * RT_LD;  // logits phase (+1 trash row)
     constexpr int P2 = RT_TOK * (EMAX + 1);            // floats, selection phase
     __shared__ __attribute__((aligned(16))) float lds[P1 > P2 ? P1 : P2];
-    float *xs = lds;                  // [RT_TOK][RT_LD]
-    float *ws = lds + RT_TOK * RT_LD; // [E][RT_LD]
+    float *xs = lds;                   // [RT_TOK][RT_LD]
+    float *ws = lds + RT_TOK * RT_LD;  // [EMAX + 1][RT_LD]
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int g = tid >> 6;                 // wave: experts [g*re, g*re + re)
-    const int re = (E + 3) / 4;
-    const int ebase = g * re;
+    const int tg = tid % RT_TG;  // tokens tg*TT .. +TT
+    const int eg = tid / RT_TG;  // experts eg*TE .. +TE
     const int64_t t0 = (int64_t)blockIdx.x * RT_TOK;
 
-    float acc[RE];
+    float acc[RT_TT][TE];
 #pragma unroll
-    for (int j = 0; j < RE; ++j) acc[j] = 0.0f;
+    for (int i = 0; i < RT_TT; ++i)
+#pragma unroll
+        for (int j = 0; j < TE; ++j) acc[i][j] = 0.0f;
 
+    // global -> register staging of one chunk: x row part (8 bf16) per
+    // thread, router floats as float4s (E*RT_HC/4 of them over 256 threads)
+    constexpr int WVEC_MAX = (EMAX * RT_HC / 4 + RT_THREADS - 1) / RT_THREADS;
     const int xtok = tid >> 2, xpart = tid & 3;
     const int64_t xt = min<int64_t>(t0 + xtok, T - 1);
     const bf16_t *xrow = x + xt * H + xpart * 8;
-
+    const int wvecs = E * (RT_HC / 4);
+    // the next chunk is held in registers across the multiply of this one
+    uint4 xr = *reinterpret_cast<const uint4 *>(xrow);
+    float4 wrg[WVEC_MAX];
+#pragma unroll
+    for (int i = 0; i < WVEC_MAX; ++i) {
+        const int c = min(tid + i * RT_THREADS, wvecs - 1);
+        const int e = c / (RT_HC / 4), part = c % (RT_HC / 4);
+        wrg[i] = *reinterpret_cast<const float4 *>(wr + (int64_t)e * H + part * 4);
+    }
     for (int h0 = 0; h0 < H; h0 += RT_HC) {
+        __syncthreads();  // previous chunk fully consumed
         {
-            const uint4 v = *reinterpret_cast<const uint4 *>(xrow + h0);
-            float4 a = make_float4(bf16_lo(v.x), bf16_hi(v.x), bf16_lo(v.y), bf16_hi(v.y));
-            float4 b = make_float4(bf16_lo(v.z), bf16_hi(v.z), bf16_lo(v.w), bf16_hi(v.w));
+            const float4 a = make_float4(bf16_lo(xr.x), bf16_hi(xr.x), bf16_lo(xr.y), bf16_hi(xr.y));
+            const float4 b = make_float4(bf16_lo(xr.z), bf16_hi(xr.z), bf16_lo(xr.w), bf16_hi(xr.w));
             *reinterpret_cast<float4 *>(xs + xtok * RT_LD + xpart * 8) = a;
             *reinterpret_cast<float4 *>(xs + xtok * RT_LD + xpart * 8 + 4) = b;
         }
-        for (int c = tid; c < E * 8; c += RT_THREADS) {
-            const int e = c >> 3, part = c & 7;
-            *reinterpret_cast<float4 *>(ws + e * RT_LD + part * 4) =
-                *reinterpret_cast<const float4 *>(wr + (int64_t)e * H + h0 + part * 4);
+#pragma unroll
+        for (int i = 0; i < WVEC_MAX; ++i) {
+            // vectors past the router's end land in the trash row EMAX
+            const int c = tid + i * RT_THREADS;
+            const int e = c < wvecs ? c / (RT_HC / 4) : EMAX, part = c % (RT_HC / 4);
+            *reinterpret_cast<float4 *>(ws + e * RT_LD + part * 4) = wrg[i];
         }
         __syncthreads();
+        if (h0 + RT_HC < H) {
+            const int h1 = h0 + RT_HC;
+            xr = *reinterpret_cast<const uint4 *>(xrow + h1);
+#pragma unroll
+            for (int i = 0; i < WVEC_MAX; ++i) {
+                const int c = min(tid + i * RT_THREADS, wvecs - 1);
+                const int e = c / (RT_HC / 4), part = c % (RT_HC / 4);
+                wrg[i] = *reinterpret_cast<const float4 *>(wr + (int64_t)e * H + h1 + part * 4);
+            }
+        }
 #pragma unroll 2
         for (int hh = 0; hh < RT_HC; hh += 4) {
-            const float4 xv = *reinterpret_cast<const float4 *>(xs + lane * RT_LD + hh);
+            float4 xv[RT_TT];
 #pragma unroll
-            for (int j = 0; j < RE; ++j) {
-                if (j < re && ebase + j < E) {
-                    const float4 wv =
-                        *reinterpret_cast<const float4 *>(ws + (ebase + j) * RT_LD + hh);
-                    float a = acc[j];
-                    a = __builtin_fmaf(xv.x, wv.x, a);
-                    a = __builtin_fmaf(xv.y, wv.y, a);
-                    a = __builtin_fmaf(xv.z, wv.z, a);
-                    a = __builtin_fmaf(xv.w, wv.w, a);
-                    acc[j] = a;
+            for (int i = 0; i < RT_TT; ++i)
+                xv[i] = *reinterpret_cast<const float4 *>(xs + (tg * RT_TT + i) * RT_LD + hh);
+#pragma unroll
+            for (int j = 0; j < TE; ++j) {
+                const int e = eg * TE + j;
+                if (e < E) {
+                    const float4 wv = *reinterpret_cast<const float4 *>(ws + e * RT_LD + hh);
+#pragma unroll
+                    for (int i = 0; i < RT_TT; ++i) {
+                        float a = acc[i][j];
+                        a = __builtin_fmaf(xv[i].x, wv.x, a);
+                        a = __builtin_fmaf(xv[i].y, wv.y, a);
+                        a = __builtin_fmaf(xv[i].z, wv.z, a);
+                        a = __builtin_fmaf(xv[i].w, wv.w, a);
+                        acc[i][j] = a;
+                    }
                 }
             }
         }
-        __syncthreads();
     }
+    __syncthreads();
 
     // ---- logits to LDS: zs[token][e], row stride EMAX+1 (odd: no conflicts)
     float *zs = lds;
     constexpr int ZLD = EMAX + 1;
 #pragma unroll
-    for (int j = 0; j < RE; ++j) {
-        const int e = ebase + j;
-        if (j < re && e < E) {
-            float z = acc[j];
-            if (bias) z = z + bias[e];
-            zs[lane * ZLD + e] = z;
+    for (int j = 0; j < TE; ++j) {
+        const int e = eg * TE + j;
+        if (e < E) {
+            const float b = bias ? bias[e] : 0.0f;
+#pragma unroll
+            for (int i = 0; i < RT_TT; ++i) {
+                float z = acc[i][j];
+                if (bias) z = z + b;
+                zs[(tg * RT_TT + i) * ZLD + e] = z;
+            }
         }
     }
     __syncthreads();
 
     // ---- selection: wave g handles tokens [g*16, g*16+16)
+    const int g = tid >> 6;
     for (int tt = g * 16; tt < g * 16 + 16; ++tt) {
         const int64_t t = t0 + tt;
         if (t >= T) break;
@@ -224,11 +270,11 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
     }
 }
 
-template <int RE>
-hipError_t launch_re(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
+template <int TE>
+hipError_t launch_te(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                      int32_t *ids, float *w, hipStream_t s) {
     const int64_t blocks = (d.tokens + RT_TOK - 1) / RT_TOK;
-    route_kernel<RE><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
+    route_kernel<TE><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
         x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
     return hipGetLastError();
 }
@@ -238,14 +284,13 @@ hipError_t launch_re(const moe_dims &d, const bf16_t *x, const float *wr, const 
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                         int32_t *ids, float *w, hipStream_t s) {
     if (d.tokens <= 0) return hipSuccess;
-    const int re = (d.experts + 3) / 4;
-    if (re <= 2) return launch_re<2>(d, x, wr, bias, ids, w, s);
-    if (re <= 4) return launch_re<4>(d, x, wr, bias, ids, w, s);
-    if (re <= 8) return launch_re<8>(d, x, wr, bias, ids, w, s);
-    if (re <= 16) return launch_re<16>(d, x, wr, bias, ids, w, s);
-    if (re <= 32) return launch_re<32>(d, x, wr, bias, ids, w, s);
-    if (re <= 48) return launch_re<48>(d, x, wr, bias, ids, w, s);
-    return launch_re<64>(d, x, wr, bias, ids, w, s);
+    const int te = (d.experts + RT_EG - 1) / RT_EG;
+    if (te <= 1) return launch_te<1>(d, x, wr, bias, ids, w, s);
+    if (te <= 2) return launch_te<2>(d, x, wr, bias, ids, w, s);
+    if (te <= 4) return launch_te<4>(d, x, wr, bias, ids, w, s);
+    if (te <= 8) return launch_te<8>(d, x, wr, bias, ids, w, s);
+    if (te <= 10) return launch_te<10>(d, x, wr, bias, ids, w, s);
+    return launch_te<16>(d, x, wr, bias, ids, w, s);
 }
 
 }  // namespace moe

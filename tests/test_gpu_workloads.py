@@ -1,0 +1,71 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times (moe_ffn_forward).  Routing, counts and the permutation are
+compared element by element with the oracle on every token; the FFN output
+on a sample of tokens the oracle computes one by one (full-size oracle FFNs
+take minutes on the host)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2410_12247_amd import moe, synth
+
+from gpu_util import Dev, assert_close
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+WORKLOADS = [("tiny", None), ("mixtral", None), ("dbrx", None), ("dsv2", None),
+             ("zipf", 64), ("zipf", 4096), ("zipf", 65536)]
+SAMPLE = 24  # tokens per workload checked against the oracle FFN
+
+
+def _shape(name, T):
+    s = synth.SHAPES[name]
+    return s.with_tokens(T) if T else s
+
+
+def _sample_tokens(T, counts_of_token, rng):
+    """First and last token, tokens with no local expert and with several,
+    plus random ones."""
+    pick = {0, T - 1}
+    none = np.flatnonzero(counts_of_token == 0)
+    many = np.flatnonzero(counts_of_token == counts_of_token.max())
+    if len(none):
+        pick.add(int(none[0]))
+    pick.add(int(many[0]))
+    while len(pick) < min(SAMPLE, T):
+        pick.add(int(rng.integers(0, T)))
+    return np.array(sorted(pick))
+
+
+@pytest.mark.parametrize("name,T", WORKLOADS, ids=[f"{n}{t or ''}" for n, t in WORKLOADS])
+def test_full_workload(name, T):
+    shp = _shape(name, T)
+    inp = synth.make_inputs(shp)
+    g = Dev(inp)
+    buf = g.forward(moe.opts(gemm_mode=moe.GEMM_AUTO, pipeline_n=1))
+    ids_g = buf.topk_ids.cpu().numpy()
+    w_g = buf.topk_w.cpu().numpy()
+    y = buf.y
+
+    # routing and dispatch of every token, bit for bit
+    _, ids, w = oracle.route(inp.x, inp.w_router, inp.bias, shp.k, shp.renorm)
+    assert np.array_equal(ids_g, ids)
+    assert np.all(np.abs(w_g.astype(np.float64) - w) <= 2.0 ** -23 * np.abs(w) + 1e-30)
+    counts, offsets, sorted_slot, slot_row = oracle.dispatch(ids, shp.e0, shp.EL)
+    assert np.array_equal(buf.counts.cpu().numpy(), counts)
+
+    # FFN output on sampled tokens
+    loc = (ids >= shp.e0) & (ids < shp.e0 + shp.EL)
+    rng = np.random.default_rng(shp.T)
+    tok = _sample_tokens(shp.T, loc.sum(1), rng)
+    ref = oracle.moe_tokens(inp.x, ids, w, tok, inp.w_gate, inp.w_up, inp.w_down, shp.e0,
+                            shp.n_shared, inp.shared_gate, inp.shared_up, inp.shared_down)
+    got = y[torch.from_numpy(tok).to(y.device)].cpu().numpy()
+    assert_close(got, ref, f"{name} T={shp.T} sampled tokens")
+
+    # the other GEMM kind and a pipelined run give the same bits
+    pn = 2 if shp.EL % 2 == 0 else 1
+    for mode in (moe.GEMM_GROUP, moe.GEMM_DENSE):
+        y2 = g.forward(moe.opts(gemm_mode=mode, pipeline_n=pn)).y
+        assert torch.equal(y2, y), f"mode {mode} PN {pn} changes the bits"

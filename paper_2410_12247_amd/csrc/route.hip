@@ -17,7 +17,9 @@
 namespace moe {
 namespace {
 
-constexpr int RT_TOK = 64;  // tokens per workgroup
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void gbl_void_t;
+
 constexpr int RT_HC = 32;   // h per LDS chunk
 constexpr int RT_LD = RT_HC + 4;
 constexpr int RT_THREADS = 256;
@@ -95,33 +97,38 @@ __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // Logits phase layout: 256 threads = 16 token groups x 16 expert groups;
-// a thread owns TT = 4 tokens x TE experts (TE = ceil(E / 16)) and keeps
-// their fma chains in registers.  x and the router are staged through LDS
-// RT_HC h at a time (the next chunk is fetched into registers while the
-// current one is multiplied); per 4 h a thread reads TT + TE float4 and
-// issues 4*TT*TE fmas.
-constexpr int RT_TT = 4;   // tokens per thread
+// a thread owns TT tokens (tg + 16 i: consecutive lanes read rows 36 floats
+// apart, so eight lanes of a 16-byte LDS read land on distinct banks) x TE
+// experts (TE = ceil(E / 16)) and keeps their fma chains in registers.  x
+// and the router are staged through two LDS buffers RT_HC h at a time: the
+// router rows by LDS-DMA, x through registers (widened to fp32), the next
+// chunk in flight while the current one is multiplied; per 4 h a thread
+// reads TT + TE float4 and issues 4*TT*TE fmas.
 constexpr int RT_TG = 16;  // token groups
 constexpr int RT_EG = 16;  // expert groups
-static_assert(RT_TT * RT_TG == RT_TOK, "token tiling");
 
-template <int TE>
+// TT tokens per thread, so a workgroup routes 16*TT tokens; the launcher
+// picks TT so that the grid keeps several workgroups per compute unit.
+template <int TE, int TT>
 __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restrict__ x,
                                                            const float *__restrict__ wr,
                                                            const float *__restrict__ bias,
                                                            int64_t T, int H, int E, int k,
                                                            int renorm, int32_t *__restrict__ ids,
                                                            float *__restrict__ wout) {
+    constexpr int RT_TOK = RT_TG * TT;  // tokens per workgroup
+    constexpr int RT_TT = TT;
     constexpr int EMAX = RT_EG * TE;
-    constexpr int P1 = RT_TOK * RT_LD + (EMAX + 1) * RT_LD;  // logits phase (+1 trash row)
-    constexpr int P2 = RT_TOK * (EMAX + 1);            // floats, selection phase
+    constexpr int XS = RT_TOK * RT_LD;  // floats of one x stage
+    constexpr int WS = EMAX * RT_HC;    // floats of one router stage (128-byte rows)
+    constexpr int P1 = 2 * XS + 2 * WS;
+    constexpr int P2 = RT_TOK * (EMAX + 1);  // selection phase
     __shared__ __attribute__((aligned(16))) float lds[P1 > P2 ? P1 : P2];
-    float *xs = lds;                   // [RT_TOK][RT_LD]
-    float *ws = lds + RT_TOK * RT_LD;  // [EMAX + 1][RT_LD]
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int tg = tid % RT_TG;  // tokens tg*TT .. +TT
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int tg = tid % RT_TG;  // tokens tg + RT_TG*i, i < TT
     const int eg = tid / RT_TG;  // experts eg*TE .. +TE
     const int64_t t0 = (int64_t)blockIdx.x * RT_TOK;
 
@@ -131,68 +138,66 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
 #pragma unroll
         for (int j = 0; j < TE; ++j) acc[i][j] = 0.0f;
 
-    // global -> register staging of one chunk: x row part (8 bf16) per
-    // thread, router floats as float4s (E*RT_HC/4 of them over 256 threads)
-    constexpr int WVEC_MAX = (EMAX * RT_HC / 4 + RT_THREADS - 1) / RT_THREADS;
-    const int xtok = tid >> 2, xpart = tid & 3;
+    // x: one 16-byte (8 bf16) piece per thread, widened to fp32 in LDS
+    const int xtok = (tid >> 2) % RT_TOK, xpart = tid & 3;  // threads past 4*TB repeat rows
     const int64_t xt = min<int64_t>(t0 + xtok, T - 1);
     const bf16_t *xrow = x + xt * H + xpart * 8;
-    const int wvecs = E * (RT_HC / 4);
-    // the next chunk is held in registers across the multiply of this one
+    // router: LDS-DMA of 8 rows x 128 bytes per wave-wide instruction;
+    // 16-byte chunk c of row r sits at chunk c ^ (r & 7)
+    const int n_wdma = (E + 7) / 8;
+    const int drow = lane >> 3;
+    const int dchunk = (lane & 7) ^ (drow & 7);
+    auto issue_w = [&](int h0, float *wsb) {
+        for (int q = wave; q < n_wdma; q += RT_THREADS / 64) {
+            const int r = min(q * 8 + drow, E - 1);  // rows past E: a copy, never read
+            __builtin_amdgcn_global_load_lds(
+                (gbl_void_t *)(wr + (int64_t)r * H + h0 + dchunk * 4),
+                (lds_void_t *)(wsb + q * 8 * RT_HC), 16, 0, 0);
+        }
+    };
+
     uint4 xr = *reinterpret_cast<const uint4 *>(xrow);
-    float4 wrg[WVEC_MAX];
-#pragma unroll
-    for (int i = 0; i < WVEC_MAX; ++i) {
-        const int c = min(tid + i * RT_THREADS, wvecs - 1);
-        const int e = c / (RT_HC / 4), part = c % (RT_HC / 4);
-        wrg[i] = *reinterpret_cast<const float4 *>(wr + (int64_t)e * H + part * 4);
-    }
-    for (int h0 = 0; h0 < H; h0 += RT_HC) {
-        __syncthreads();  // previous chunk fully consumed
+    issue_w(0, lds + 2 * XS);
+    const int nchunk = H / RT_HC;
+    for (int c = 0; c < nchunk; ++c) {
+        const int st = c & 1;
+        float *xs = lds + st * XS;
+        const float *ws = lds + 2 * XS + st * WS;
         {
             const float4 a = make_float4(bf16_lo(xr.x), bf16_hi(xr.x), bf16_lo(xr.y), bf16_hi(xr.y));
             const float4 b = make_float4(bf16_lo(xr.z), bf16_hi(xr.z), bf16_lo(xr.w), bf16_hi(xr.w));
             *reinterpret_cast<float4 *>(xs + xtok * RT_LD + xpart * 8) = a;
             *reinterpret_cast<float4 *>(xs + xtok * RT_LD + xpart * 8 + 4) = b;
         }
-#pragma unroll
-        for (int i = 0; i < WVEC_MAX; ++i) {
-            // vectors past the router's end land in the trash row EMAX
-            const int c = tid + i * RT_THREADS;
-            const int e = c < wvecs ? c / (RT_HC / 4) : EMAX, part = c % (RT_HC / 4);
-            *reinterpret_cast<float4 *>(ws + e * RT_LD + part * 4) = wrg[i];
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this chunk's router rows landed
+        __syncthreads();  // ... for every wave; chunk c-1 fully consumed
+        if (c + 1 < nchunk) {
+            xr = *reinterpret_cast<const uint4 *>(xrow + (c + 1) * RT_HC);
+            issue_w((c + 1) * RT_HC, lds + 2 * XS + (st ^ 1) * WS);
         }
-        __syncthreads();
-        if (h0 + RT_HC < H) {
-            const int h1 = h0 + RT_HC;
-            xr = *reinterpret_cast<const uint4 *>(xrow + h1);
 #pragma unroll
-            for (int i = 0; i < WVEC_MAX; ++i) {
-                const int c = min(tid + i * RT_THREADS, wvecs - 1);
-                const int e = c / (RT_HC / 4), part = c % (RT_HC / 4);
-                wrg[i] = *reinterpret_cast<const float4 *>(wr + (int64_t)e * H + h1 + part * 4);
-            }
-        }
-#pragma unroll 2
         for (int hh = 0; hh < RT_HC; hh += 4) {
-            float4 xv[RT_TT];
+            // all operands of this 4-h step first, then the fmas
+            float4 xv[RT_TT], wv[TE];
 #pragma unroll
             for (int i = 0; i < RT_TT; ++i)
-                xv[i] = *reinterpret_cast<const float4 *>(xs + (tg * RT_TT + i) * RT_LD + hh);
+                xv[i] = *reinterpret_cast<const float4 *>(xs + (tg + RT_TG * i) * RT_LD + hh);
 #pragma unroll
             for (int j = 0; j < TE; ++j) {
-                const int e = eg * TE + j;
-                if (e < E) {
-                    const float4 wv = *reinterpret_cast<const float4 *>(ws + e * RT_LD + hh);
+                const int e = min(eg * TE + j, EMAX - 1);
+                wv[j] = *reinterpret_cast<const float4 *>(ws + e * RT_HC +
+                                                          (((hh >> 2) ^ (e & 7)) << 2));
+            }
 #pragma unroll
-                    for (int i = 0; i < RT_TT; ++i) {
-                        float a = acc[i][j];
-                        a = __builtin_fmaf(xv[i].x, wv.x, a);
-                        a = __builtin_fmaf(xv[i].y, wv.y, a);
-                        a = __builtin_fmaf(xv[i].z, wv.z, a);
-                        a = __builtin_fmaf(xv[i].w, wv.w, a);
-                        acc[i][j] = a;
-                    }
+            for (int j = 0; j < TE; ++j) {
+#pragma unroll
+                for (int i = 0; i < RT_TT; ++i) {
+                    float v = acc[i][j];
+                    v = __builtin_fmaf(xv[i].x, wv[j].x, v);
+                    v = __builtin_fmaf(xv[i].y, wv[j].y, v);
+                    v = __builtin_fmaf(xv[i].z, wv[j].z, v);
+                    v = __builtin_fmaf(xv[i].w, wv[j].w, v);
+                    acc[i][j] = v;
                 }
             }
         }
@@ -211,15 +216,15 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
             for (int i = 0; i < RT_TT; ++i) {
                 float z = acc[i][j];
                 if (bias) z = z + b;
-                zs[(tg * RT_TT + i) * ZLD + e] = z;
+                zs[(tg + RT_TG * i) * ZLD + e] = z;
             }
         }
     }
     __syncthreads();
 
-    // ---- selection: wave g handles tokens [g*16, g*16+16)
+    // ---- selection: wave g handles tokens [g*TB/4, (g+1)*TB/4)
     const int g = tid >> 6;
-    for (int tt = g * 16; tt < g * 16 + 16; ++tt) {
+    for (int tt = g * (RT_TOK / 4); tt < (g + 1) * (RT_TOK / 4); ++tt) {
         const int64_t t = t0 + tt;
         if (t >= T) break;
         uint64_t key[4];
@@ -270,13 +275,24 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
     }
 }
 
+template <int TE, int TT>
+hipError_t launch_tt(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
+                     int32_t *ids, float *w, hipStream_t s) {
+    const int64_t blocks = (d.tokens + RT_TG * TT - 1) / (RT_TG * TT);
+    route_kernel<TE, TT><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
+        x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
+    return hipGetLastError();
+}
+
 template <int TE>
 hipError_t launch_te(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                      int32_t *ids, float *w, hipStream_t s) {
-    const int64_t blocks = (d.tokens + RT_TOK - 1) / RT_TOK;
-    route_kernel<TE><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
-        x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
-    return hipGetLastError();
+    // the most tokens per thread (fewest LDS reads per fma) that still
+    // leaves enough workgroups per CU to hide latency
+    const int cus = device_cu_count();
+    if (d.tokens >= (int64_t)64 * 4 * cus) return launch_tt<TE, 4>(d, x, wr, bias, ids, w, s);
+    if (d.tokens >= (int64_t)32 * 2 * cus) return launch_tt<TE, 2>(d, x, wr, bias, ids, w, s);
+    return launch_tt<TE, 1>(d, x, wr, bias, ids, w, s);
 }
 
 }  // namespace

@@ -48,7 +48,10 @@ def parse_args(argv=None):
     p.add_argument("--config", default="mixtral", choices=sorted(WORKLOAD_TEXT))
     p.add_argument("--tokens", type=int, default=0, help="override T (zipf sweep point)")
     p.add_argument("--mode", default="auto", choices=["auto", "group", "dense"])
-    p.add_argument("--pn", type=int, default=1, help="pipeline number (divides local experts)")
+    p.add_argument("--pn", type=int, default=1,
+                   help="pipeline number (divides the local experts for expert stages)")
+    p.add_argument("--chunk-mode", default="experts", choices=["experts", "tokens"],
+                   help="pipeline stages: expert groups (default) or token ranges")
     p.add_argument("--cu-budget", type=int, default=0)
     p.add_argument("--dense-min-rows", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -56,6 +59,8 @@ def parse_args(argv=None):
                    help="target CPU time of the oracle baseline sample")
     p.add_argument("--sweep", action="store_true",
                    help="GroupGemm vs DenseGemm vs AUTO over the zipf token counts")
+    p.add_argument("--pn-sweep", action="store_true",
+                   help="step time over pipeline numbers and both stage kinds for --config")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                    help="only run a plain device copy of BYTES (HBM counter calibration)")
     return p.parse_args(argv)
@@ -121,8 +126,9 @@ def run_workload(args, shape, inp, steps, warmup, timing=True):
     from paper_2410_12247_amd.workload import DeviceInputs
 
     mode = {"auto": moe.GEMM_AUTO, "group": moe.GEMM_GROUP, "dense": moe.GEMM_DENSE}[args.mode]
+    chunk = {"experts": moe.CHUNK_EXPERTS, "tokens": moe.CHUNK_TOKENS}[args.chunk_mode]
     o = moe.opts(gemm_mode=mode, pipeline_n=args.pn, gemm_cu_budget=args.cu_budget,
-                 dense_min_rows=args.dense_min_rows, timing=timing)
+                 dense_min_rows=args.dense_min_rows, timing=timing, chunk_mode=chunk)
     g = DeviceInputs(inp)
     buf = g.buffers(o)
 
@@ -164,6 +170,16 @@ def measured_traffic(workload, kernel_prefix):
     return None
 
 
+def phase_bytes(s, R, accumulate):
+    """Algorithmic HBM bytes of the memory-bound phases of one forward."""
+    return {
+        "route": s.T * s.H * 2 + s.E * s.H * 4 + s.T * s.k * 8,
+        "permute": s.T * s.k * 12,
+        "gather": 2 * R * s.H * 2,
+        "combine": R * s.H * 4 + s.T * s.H * 4 * (2 if accumulate else 1) + s.T * s.k * 8,
+    }
+
+
 def summarize_timing(tms):
     keys = tms[0].keys()
     return {k: sum(t[k] for t in tms) / len(tms) for k in keys}
@@ -187,6 +203,8 @@ def main(argv=None):
     torch.cuda.set_device(0)
     if args.sweep:
         return sweep(args)
+    if args.pn_sweep:
+        return pn_sweep(args)
     shape = synth.SHAPES[args.config]
     if args.tokens:
         shape = shape.with_tokens(args.tokens)
@@ -204,6 +222,10 @@ def main(argv=None):
     per_launch_flops = fg / max(tm["gateup_launches"], 1)
     achieved = per_launch_flops / (per_launch_ms * 1e-3) / 1e12
     peak = PEAK_BF16_FLOPS / 1e12
+    pb = phase_bytes(shape, R, shape.shared_inter > 0)
+    gbps = {k: round(v / (tm[f"{k}_ms"] * 1e-3) / 1e9, 1) for k, v in pb.items()
+            if tm[f"{k}_ms"] > 0}
+    routed_ms = tm["gateup_ms"] + tm["down_ms"]
     traffic = None
     if tm["group_stages"] and not tm["dense_stages"] and args.pn == 1 and not args.tokens:
         kname = "group_kernel<0"
@@ -228,6 +250,7 @@ def main(argv=None):
                    "experts": shape.E, "local_experts": shape.EL, "top_k": shape.k,
                    "renormalize": shape.renorm, "shared_inter": shape.shared_inter,
                    "gemm_mode": args.mode, "pipeline_n": args.pn,
+                   "chunk_mode": args.chunk_mode,
                    "gemm_cu_budget": args.cu_budget, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
@@ -238,7 +261,12 @@ def main(argv=None):
         "gemm": {"tflops_per_s_wall": round(gemm_flops_total / (ms * 1e-3) / 1e12, 1),
                  "tflops_per_s_busy": round(gemm_flops_total / (gemm_ms * 1e-3) / 1e12, 1),
                  "mfma_frac_busy": round(gemm_flops_total / (gemm_ms * 1e-3) / PEAK_BF16_FLOPS, 4),
+                 "routed_mfma_frac_busy": round((fg + fd) / (routed_ms * 1e-3) / PEAK_BF16_FLOPS,
+                                                4) if routed_ms > 0 else None,
+                 "shared_mfma_frac_busy": round(fs / (tm["shared_ms"] * 1e-3) / PEAK_BF16_FLOPS,
+                                                4) if tm["shared_ms"] > 0 else None,
                  "gflop": round(gemm_flops_total / 1e9, 1), "routed_rows": R},
+        "hbm_gbps": {**gbps, "peak": PEAK_HBM_BYTES / 1e9},
         "phases_ms": {k: round(v, 4) for k, v in tm.items() if k.endswith("_ms")},
         "stages": {k: tm[k] for k in ("dense_stages", "group_stages")},
     }
@@ -272,6 +300,34 @@ def sweep(args):
                           "gemm_gflop": round((fg + fd) / 1e9, 2), **res,
                           "auto_regret": round(res["auto"]["gemm_ms"] / best - 1, 4)}),
               flush=True)
+    return 0
+
+
+def pn_sweep(args):
+    """Step time of --config over pipeline numbers, with expert-group stages
+    (PN dividing the local experts) and token-range stages; one JSON line per
+    point, each with the per-phase device times summed over stages."""
+    from paper_2410_12247_amd import synth
+
+    shape = synth.SHAPES[args.config]
+    if args.tokens:
+        shape = shape.with_tokens(args.tokens)
+    inp = synth.make_inputs(shape)
+    for chunk in ("experts", "tokens"):
+        for pn in (1, 2, 4, 5, 8, 10, 20):
+            if chunk == "experts" and shape.EL % pn:
+                continue
+            if chunk == "tokens" and (pn == 1 or pn * shape.EL > 256):
+                continue
+            a = argparse.Namespace(**{**vars(args), "pn": pn, "chunk_mode": chunk})
+            wall, tms, counts = run_workload(a, shape, inp, args.steps, args.warmup)
+            tm = summarize_timing(tms)
+            wall_u, _, _ = run_workload(a, shape, inp, args.steps, args.warmup, timing=False)
+            print(json.dumps({"pn_sweep": args.config, "tokens": shape.T, "chunk_mode": chunk,
+                              "pipeline_n": pn, "gemm_mode": args.mode,
+                              "ms_per_step": round(wall_u / args.steps * 1e3, 4),
+                              "phases_ms": {k: round(v, 4) for k, v in tm.items()
+                                            if k.endswith("_ms")}}), flush=True)
     return 0
 
 

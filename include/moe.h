@@ -65,23 +65,34 @@ typedef struct {
 } moe_dims;
 
 enum { MOE_GEMM_AUTO = 0, MOE_GEMM_GROUP = 1, MOE_GEMM_DENSE = 2 };
+enum { MOE_CHUNK_EXPERTS = 0, MOE_CHUNK_TOKENS = 1 };
 enum { MOE_FLAG_TIMING = 1 };
 
 /* Options of moe_ffn_forward (Sec. 4.3 of the paper: the GroupGemm /
- * DenseGemm switch by load and the pipeline number PN). */
+ * DenseGemm switch by load, the pipeline number PN and how the work is cut
+ * into pipeline stages).
+ * chunk_mode MOE_CHUNK_EXPERTS (default): stage s is the expert group
+ *   [s*EL/PN, (s+1)*EL/PN) with all of its rows, so each expert's weights
+ *   are read by one stage only (the paper's horizontal split with weights
+ *   split by expert, Sec. 4.3).  PN must divide local_count.
+ * chunk_mode MOE_CHUNK_TOKENS: stage s is the token range
+ *   [s*ceil(T/PN), (s+1)*ceil(T/PN)) over all local experts, so every stage
+ *   reads every local expert's weights again (the split the paper argues
+ *   against); kept as a measured comparison.  Needs PN*local_count <= 256.
+ * Both modes give the same bits. */
 typedef struct {
     int32_t gemm_mode;      /* MOE_GEMM_AUTO, _GROUP or _DENSE */
     int32_t dense_min_rows; /* AUTO picks DenseGemm for a pipeline stage when
                                every expert in it has at least this many
                                rows, else GroupGemm; 0 = built-in default
                                (see moe_default_dense_min_rows) */
-    int32_t pipeline_n;     /* PN >= 1, must divide local_count: stage s owns
-                               local experts [s*EL/PN, (s+1)*EL/PN) */
+    int32_t pipeline_n;     /* PN >= 1, the number of pipeline stages */
     int32_t gemm_cu_budget; /* workgroups of the persistent grouped GEMM;
                                0 = one per compute unit */
     int32_t flags;          /* MOE_FLAG_TIMING: time each phase with HIP
                                events (read with moe_last_timing) */
-    int32_t reserved[3];    /* must be zero */
+    int32_t chunk_mode;     /* MOE_CHUNK_EXPERTS or MOE_CHUNK_TOKENS */
+    int32_t reserved[2];    /* must be zero */
 } moe_opts;
 
 /* Per-phase device time of the last moe_ffn_forward call on this thread
@@ -94,8 +105,9 @@ typedef struct {
 } moe_timing;
 
 /* Bytes of device workspace: with opts == NULL, what moe_permute needs;
- * with opts != NULL, what moe_ffn_forward needs (a superset).  Host-only;
- * never touches the GPU.  Returns 0 for invalid dims. */
+ * with opts != NULL, what moe_ffn_forward needs with those options (a
+ * superset).  Host-only; never touches the GPU.  Returns 0 for invalid dims
+ * or options. */
 size_t moe_workspace_bytes(const moe_dims *dims, const moe_opts *opts);
 
 /* Router (the topKGating operator of Sec. 3.3; k of E experts per token as

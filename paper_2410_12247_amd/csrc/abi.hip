@@ -60,10 +60,12 @@ moe_status check_dims(const moe_dims *d) {
     return MOE_OK;
 }
 
-WsLayout ws_layout(const moe_dims *d, bool forward) {
+WsLayout ws_layout(const moe_dims *d, bool forward, int nbuckets) {
     WsLayout L{};
     const int64_t T = d->tokens, k = d->top_k, EL = d->local_count;
     const int64_t nslots = T * k;
+    const int64_t NB = nbuckets;
+    L.nbuckets = nbuckets;
     L.nchunks = (nslots + kPermChunk - 1) / kPermChunk;
     L.rcap = T * (k < EL ? k : EL);
     size_t o = 0;
@@ -72,14 +74,15 @@ WsLayout ws_layout(const moe_dims *d, bool forward) {
         o = align_up(o + bytes);
         return at;
     };
-    L.chunk_counts = take(sizeof(int32_t) * L.nchunks * EL);
-    L.chunk_base = take(sizeof(int32_t) * L.nchunks * EL);
+    L.chunk_counts = take(sizeof(int32_t) * L.nchunks * NB);
+    L.chunk_base = take(sizeof(int32_t) * L.nchunks * NB);
     L.slot_rank = take(sizeof(int32_t) * nslots);
     if (forward) {
         L.ids = take(sizeof(int32_t) * nslots);
         L.weights = take(sizeof(float) * nslots);
-        L.counts = take(sizeof(int32_t) * EL);
-        L.offsets = take(sizeof(int32_t) * (EL + 1));
+        L.counts = take(sizeof(int32_t) * NB);
+        L.counts_el = take(sizeof(int32_t) * EL);
+        L.offsets = take(sizeof(int32_t) * (NB + 1));
         L.sorted_slot = take(sizeof(int32_t) * L.rcap);
         L.slot_row = take(sizeof(int32_t) * nslots);
         L.x_perm = take(sizeof(bf16_t) * L.rcap * d->hidden);
@@ -128,9 +131,10 @@ const char *moe_status_string(moe_status s) {
 const char *moe_last_error(void) { return g_last_error; }
 
 size_t moe_workspace_bytes(const moe_dims *dims, const moe_opts *opts) {
-    (void)opts;
     if (check_dims(dims) != MOE_OK) return 0;
-    return ws_layout(dims, opts != nullptr).total;
+    if (!opts) return ws_layout(dims, false, dims->local_count).total;
+    const int nb = forward_buckets(dims, opts);
+    return nb > 0 ? ws_layout(dims, true, nb).total : 0;
 }
 
 moe_status moe_route(const moe_dims *dims, const moe_bf16 *x, const float *w_router,
@@ -152,12 +156,13 @@ moe_status moe_permute(const moe_dims *dims, const int32_t *topk_ids, const moe_
     if (!topk_ids || !counts || !offsets || !sorted_slot || !slot_row)
         return fail(MOE_ERR_INVALID, "moe_permute: NULL index tensor");
     if (x_perm && !x) return fail(MOE_ERR_INVALID, "moe_permute: x_perm given without x");
-    const WsLayout L = ws_layout(dims, false);
+    const WsLayout L = ws_layout(dims, false, dims->local_count);
     if (!ws || ws_bytes < L.total)
         return fail(MOE_ERR_WORKSPACE, "moe_permute: workspace %zu < %zu bytes", ws_bytes,
                     L.total);
     hipStream_t s = (hipStream_t)stream;
-    MOE_HIP(launch_permute(*dims, topk_ids, ws, L, counts, offsets, sorted_slot, slot_row, s));
+    MOE_HIP(launch_permute(*dims, topk_ids, ws, L, 0, counts, offsets, nullptr, sorted_slot,
+                           slot_row, s));
     if (x_perm)
         MOE_HIP(launch_gather(*dims, 0, dims->local_count, offsets, sorted_slot, x, x_perm,
                               L.rcap, s));
@@ -228,8 +233,8 @@ moe_status moe_combine(const moe_dims *dims, int32_t e_first, int32_t e_count,
     if (dims->tokens == 0) return MOE_OK;
     if (!topk_ids || !slot_row || !topk_w || !y || (!y_perm && e_count > 0))
         return fail(MOE_ERR_INVALID, "moe_combine: NULL tensor");
-    MOE_HIP(launch_combine(*dims, e_first, e_count, y_perm, topk_ids, slot_row, topk_w, y,
-                           accumulate, (hipStream_t)stream));
+    MOE_HIP(launch_combine(*dims, e_first, e_count, 0, dims->tokens, y_perm, topk_ids, slot_row,
+                           topk_w, y, accumulate, (hipStream_t)stream));
     return MOE_OK;
 }
 

@@ -1,8 +1,9 @@
 // Combine (LocalReduce): y[t] (+)= sum_j w[t][j] * y_perm[slot_row[t*k+j]]
-// over the token's slots whose local expert lies in [e_first, e_first +
-// e_count), terms in ascending expert order, one fp32 fma each.  Adding the
-// stages of a pipeline one after another therefore performs exactly the same
-// fma sequence as a single call over all experts.
+// for tokens t in [t_begin, t_end) over the token's slots whose local
+// expert lies in [e_first, e_first + e_count), terms in ascending expert
+// order, one fp32 fma each.  Adding the stages of a pipeline one after
+// another therefore performs exactly the same fma sequence as a single call
+// over all experts and tokens.
 //
 // One wave per token: the wave reads the token's k slot records, orders the
 // selected ones by expert id (each ranked by counting smaller ids), then streams
@@ -12,7 +13,8 @@
 namespace moe {
 namespace {
 
-__global__ __launch_bounds__(256) void combine_kernel(int64_t T, int H, int k, int e0,
+__global__ __launch_bounds__(256) void combine_kernel(int64_t t_begin, int64_t t_end, int H,
+                                                      int k, int e0,
                                                       int e_lo, int e_hi,
                                                       const float *__restrict__ y_perm,
                                                       const int32_t *__restrict__ ids,
@@ -20,8 +22,8 @@ __global__ __launch_bounds__(256) void combine_kernel(int64_t T, int H, int k, i
                                                       const float *__restrict__ w,
                                                       float *__restrict__ y, int accumulate) {
     const int lane = threadIdx.x & 63;
-    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (t >= T) return;
+    const int64_t t = t_begin + (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (t >= t_end) return;
     // slot records of this token (wave-uniform after readlane)
     int my_e = 1 << 30, my_r = -1;
     float my_w = 0.f;
@@ -91,14 +93,15 @@ __global__ __launch_bounds__(256) void combine_kernel(int64_t T, int H, int k, i
 
 }  // namespace
 
-hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, const float *y_perm,
-                          const int32_t *ids, const int32_t *slot_row, const float *w,
-                          float *y, int accumulate, hipStream_t s) {
-    if (d.tokens <= 0) return hipSuccess;
-    const int64_t blocks = (d.tokens + 3) / 4;
-    combine_kernel<<<(unsigned)blocks, 256, 0, s>>>(d.tokens, d.hidden, d.top_k, d.local_begin,
-                                                    e_first, e_first + e_count, y_perm, ids,
-                                                    slot_row, w, y, accumulate);
+hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, int64_t t_begin,
+                          int64_t t_end, const float *y_perm, const int32_t *ids,
+                          const int32_t *slot_row, const float *w, float *y, int accumulate,
+                          hipStream_t s) {
+    if (t_end <= t_begin) return hipSuccess;
+    const int64_t blocks = (t_end - t_begin + 3) / 4;
+    combine_kernel<<<(unsigned)blocks, 256, 0, s>>>(t_begin, t_end, d.hidden, d.top_k,
+                                                    d.local_begin, e_first, e_first + e_count,
+                                                    y_perm, ids, slot_row, w, y, accumulate);
     return hipGetLastError();
 }
 

@@ -42,15 +42,18 @@ moe_status check_dims(const moe_dims *d);
 // Number of compute units of the current device (cached per device).
 int device_cu_count();
 
-// Workspace layout used by moe_permute and moe_ffn_forward.
+// Workspace layout used by moe_permute and moe_ffn_forward.  The dispatch
+// orders rows by a bucket index: the local expert (EXPERTS stages) or
+// token-range stage * EL + local expert (TOKENS stages); nbuckets of them.
 struct WsLayout {
-    size_t chunk_counts;  // int32 [nchunks][EL]
-    size_t chunk_base;    // int32 [nchunks][EL]
+    size_t chunk_counts;  // int32 [nchunks][nbuckets]
+    size_t chunk_base;    // int32 [nchunks][nbuckets]
     size_t slot_rank;     // int32 [T*k]
     size_t ids;           // int32 [T*k]   (forward, when the caller passes none)
     size_t weights;       // fp32  [T*k]
-    size_t counts;        // int32 [EL]
-    size_t offsets;       // int32 [EL+1]
+    size_t counts;        // int32 [nbuckets] rows per bucket
+    size_t counts_el;     // int32 [EL] rows per local expert (TOKENS stages)
+    size_t offsets;       // int32 [nbuckets+1]
     size_t sorted_slot;   // int32 [Rcap]
     size_t slot_row;      // int32 [T*k]
     size_t x_perm;        // bf16  [Rcap][H]
@@ -60,8 +63,12 @@ struct WsLayout {
     size_t total;
     int64_t nchunks;
     int64_t rcap;
+    int nbuckets;
 };
-WsLayout ws_layout(const moe_dims *d, bool forward);
+WsLayout ws_layout(const moe_dims *d, bool forward, int nbuckets);
+// Dispatch buckets moe_ffn_forward uses with options o (EL, or PN*EL for
+// token-range stages); 0 when the options are not usable.
+int forward_buckets(const moe_dims *d, const moe_opts *o);
 
 // Permutation chunking: slots handled by one workgroup of the histogram pass.
 constexpr int kPermChunk = 1024;
@@ -69,15 +76,22 @@ constexpr int kPermChunk = 1024;
 // ---- kernel launchers (stream-ordered, no host synchronisation) ----------
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                         int32_t *ids, float *w, hipStream_t s);
+// Dispatch indices.  tokens_per_stage == 0: buckets are the local experts;
+// else bucket = (t / tokens_per_stage) * EL + local expert and counts_el
+// (may be NULL) receives the rows per local expert summed over stages.
 hipError_t launch_permute(const moe_dims &d, const int32_t *ids, void *ws, const WsLayout &L,
-                          int32_t *counts, int32_t *offsets, int32_t *sorted_slot,
-                          int32_t *slot_row, hipStream_t s);
+                          int64_t tokens_per_stage, int32_t *counts, int32_t *offsets,
+                          int32_t *counts_el, int32_t *sorted_slot, int32_t *slot_row,
+                          hipStream_t s);
 hipError_t launch_gather(const moe_dims &d, int e_first, int e_count, const int32_t *offsets,
                          const int32_t *sorted_slot, const bf16_t *x, bf16_t *x_perm,
                          int64_t max_rows, hipStream_t s);
-hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, const float *y_perm,
-                          const int32_t *ids, const int32_t *slot_row, const float *w,
-                          float *y, int accumulate, hipStream_t s);
+// Combine of the local experts [e_first, e_first+e_count) for the tokens
+// [t_begin, t_end).
+hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, int64_t t_begin,
+                          int64_t t_end, const float *y_perm, const int32_t *ids,
+                          const int32_t *slot_row, const float *w, float *y, int accumulate,
+                          hipStream_t s);
 // Grouped GEMMs over local experts [e_first, e_first+e_count) (rows from
 // device offsets).  max_rows bounds the rows of the range (for grid sizing
 // only; pass T*min(k,EL) when unknown).

@@ -4,16 +4,19 @@
 // Streams (per device, created once, default priority):
 //   caller stream s0 : route, dispatch indices, the host copy of counts
 //   sg (gather)      : stage i's row gather (the one-GPU stand-in for the
-//                      dispatch all2all of one expert group)
+//                      dispatch all2all of one stage)
 //   sm (GEMM)        : shared experts, then each stage's expert GEMMs
 //   sc (combine)     : each stage's weighted combine, in stage order
 // Stage i's GEMMs wait for its gather; its combine waits for its GEMMs, so
-// gather(i+1) and combine(i-1) overlap GEMM(i).  A stage is an expert
-// group: local experts [i*EL/PN, (i+1)*EL/PN), whose rows are one contiguous
-// range of the expert-sorted buffers, so each expert's weights are read by
-// exactly one stage (the paper's horizontal split with weights split by
-// expert, Sec. 4.3).  The GEMM kind of each stage is chosen from its row
-// counts (GroupGemm for small loads, DenseGemm per expert for large ones).
+// gather(i+1) and combine(i-1) overlap GEMM(i).  By default a stage is an
+// expert group: local experts [i*EL/PN, (i+1)*EL/PN), whose rows are one
+// contiguous range of the expert-sorted buffers, so each expert's weights
+// are read by exactly one stage (the paper's horizontal split with weights
+// split by expert, Sec. 4.3).  With token-range stages the dispatch orders
+// rows by (stage, expert, token) instead, so stage i's rows are again one
+// contiguous range, now covering every expert.  The GEMM kind of each stage
+// is chosen from its row counts (GroupGemm for small loads, DenseGemm per
+// expert for large ones).
 #include <algorithm>
 #include <mutex>
 #include <vector>
@@ -126,17 +129,30 @@ moe_status check_opts(const moe_dims *d, const moe_opts *o) {
     if (o->gemm_mode < MOE_GEMM_AUTO || o->gemm_mode > MOE_GEMM_DENSE)
         return fail(MOE_ERR_INVALID, "gemm_mode %d unknown", o->gemm_mode);
     if (o->dense_min_rows < 0) return fail(MOE_ERR_INVALID, "dense_min_rows < 0");
-    if (o->pipeline_n < 1 || d->local_count % o->pipeline_n)
-        return fail(MOE_ERR_INVALID, "pipeline_n %d must be >= 1 and divide local_count %d",
+    if (o->chunk_mode != MOE_CHUNK_EXPERTS && o->chunk_mode != MOE_CHUNK_TOKENS)
+        return fail(MOE_ERR_INVALID, "chunk_mode %d unknown", o->chunk_mode);
+    if (o->pipeline_n < 1) return fail(MOE_ERR_INVALID, "pipeline_n %d < 1", o->pipeline_n);
+    if (o->chunk_mode == MOE_CHUNK_EXPERTS && d->local_count % o->pipeline_n)
+        return fail(MOE_ERR_INVALID, "pipeline_n %d must divide local_count %d",
                     o->pipeline_n, d->local_count);
+    if (o->chunk_mode == MOE_CHUNK_TOKENS &&
+        (int64_t)o->pipeline_n * d->local_count > kMaxExperts)
+        return fail(MOE_ERR_UNSUPPORTED, "token stages: pipeline_n * local_count > %d",
+                    kMaxExperts);
     if (o->gemm_cu_budget < 0) return fail(MOE_ERR_INVALID, "gemm_cu_budget < 0");
     if (o->flags & ~MOE_FLAG_TIMING) return fail(MOE_ERR_INVALID, "unknown flags 0x%x", o->flags);
-    for (int i = 0; i < 3; ++i)
+    for (int i = 0; i < 2; ++i)
         if (o->reserved[i]) return fail(MOE_ERR_INVALID, "reserved options must be zero");
     return MOE_OK;
 }
 
 }  // namespace
+
+int forward_buckets(const moe_dims *d, const moe_opts *o) {
+    if (check_opts(d, o) != MOE_OK) return 0;
+    return o->chunk_mode == MOE_CHUNK_TOKENS ? o->pipeline_n * d->local_count : d->local_count;
+}
+
 }  // namespace moe
 
 using namespace moe;
@@ -164,7 +180,9 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     const bool has_shared = d.shared_inter > 0;
     if (has_shared && (!shared_gate || !shared_up || !shared_down))
         return fail(MOE_ERR_INVALID, "moe_ffn_forward: shared_inter > 0 needs shared weights");
-    const WsLayout L = ws_layout(dims, true);
+    const bool tok_stages = o->chunk_mode == MOE_CHUNK_TOKENS;
+    const int NB = forward_buckets(dims, o);
+    const WsLayout L = ws_layout(dims, true, NB);
     if (!ws || ws_bytes < L.total)
         return fail(MOE_ERR_WORKSPACE, "moe_ffn_forward: workspace %zu < %zu bytes", ws_bytes,
                     L.total);
@@ -172,7 +190,12 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     char *base = static_cast<char *>(ws);
     int32_t *ids = topk_ids ? topk_ids : reinterpret_cast<int32_t *>(base + L.ids);
     float *wts = topk_w ? topk_w : reinterpret_cast<float *>(base + L.weights);
-    int32_t *cnt = counts ? counts : reinterpret_cast<int32_t *>(base + L.counts);
+    // rows per bucket (local expert, or stage * EL + local expert) and their
+    // prefix; the caller's counts are per local expert
+    int32_t *cnt_el = counts ? counts
+                             : reinterpret_cast<int32_t *>(base + (tok_stages ? L.counts_el
+                                                                              : L.counts));
+    int32_t *cnt = tok_stages ? reinterpret_cast<int32_t *>(base + L.counts) : cnt_el;
     int32_t *off = reinterpret_cast<int32_t *>(base + L.offsets);
     int32_t *sorted_slot = reinterpret_cast<int32_t *>(base + L.sorted_slot);
     int32_t *slot_row = reinterpret_cast<int32_t *>(base + L.slot_row);
@@ -185,7 +208,8 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     MOE_TRY(get_state(&st));
     const int PN = o->pipeline_n;
     const int EL = d.local_count;
-    const int per_stage = EL / PN;
+    const int per_stage = tok_stages ? EL : EL / PN;  // buckets per stage
+    const int64_t tps = tok_stages ? (d.tokens + PN - 1) / PN : 0;
     {
         std::lock_guard<std::mutex> lock(g_mu);
         MOE_TRY(ensure_events(st->sync_ev, 3 * (size_t)PN + 4, hipEventDisableTiming));
@@ -219,7 +243,7 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     MOE_HIP(launch_route(d, x, w_router, bias, ids, wts, s0));
     MOE_TRY(tm.end(s0));
     MOE_TRY(tm.begin(s0, PH_PERMUTE));
-    MOE_HIP(launch_permute(d, ids, ws, L, cnt, off, sorted_slot, slot_row, s0));
+    MOE_HIP(launch_permute(d, ids, ws, L, tps, cnt, off, cnt_el, sorted_slot, slot_row, s0));
     MOE_TRY(tm.end(s0));
 
     // GEMM kind per stage needs the row counts on the host
@@ -232,11 +256,11 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
         o->gemm_mode == MOE_GEMM_DENSE || PN > 1 ||
         (o->gemm_mode == MOE_GEMM_AUTO && m_star <= d.tokens);
     if (need_counts) {
-        MOE_HIP(hipMemcpyAsync(st->pinned_counts, cnt, sizeof(int32_t) * EL,
+        MOE_HIP(hipMemcpyAsync(st->pinned_counts, cnt, sizeof(int32_t) * NB,
                                hipMemcpyDeviceToHost, s0));
         MOE_HIP(hipEventRecord(ev_counts, s0));
         MOE_HIP(hipEventSynchronize(ev_counts));
-        hc.assign(st->pinned_counts, st->pinned_counts + EL);
+        hc.assign(st->pinned_counts, st->pinned_counts + NB);
     }
     int grid = o->gemm_cu_budget > 0 ? o->gemm_cu_budget : device_cu_count();
     grid = std::max(8, (grid / 8) * 8);
@@ -247,21 +271,25 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     MOE_HIP(hipStreamWaitEvent(st->sc, ev_fork, 0));
 
     for (int i = 0; i < PN; ++i) {
-        const int ef = i * per_stage;
+        // buckets [b0, b0 + per_stage); their experts start at e_w (weights)
+        const int b0 = i * per_stage;
+        const int e_w = tok_stages ? 0 : b0;
+        const int64_t t_lo = tok_stages ? std::min<int64_t>(T, i * tps) : 0;
+        const int64_t t_hi = tok_stages ? std::min<int64_t>(T, (i + 1) * tps) : T;
         int64_t stage_rows = L.rcap;
         bool dense = o->gemm_mode == MOE_GEMM_DENSE;
         if (need_counts) {
             stage_rows = 0;
             int32_t min_rows = INT32_MAX;
-            for (int e = ef; e < ef + per_stage; ++e) {
-                stage_rows += hc[e];
-                min_rows = std::min(min_rows, hc[e]);
+            for (int b = b0; b < b0 + per_stage; ++b) {
+                stage_rows += hc[b];
+                min_rows = std::min(min_rows, hc[b]);
             }
             if (o->gemm_mode == MOE_GEMM_AUTO) dense = min_rows >= m_star;
         }
-        // gather (dispatch of this expert group)
+        // gather (dispatch of this stage)
         MOE_TRY(tm.begin(st->sg, PH_GATHER));
-        MOE_HIP(launch_gather(d, ef, per_stage, off, sorted_slot, x, x_perm, stage_rows, st->sg));
+        MOE_HIP(launch_gather(d, b0, per_stage, off, sorted_slot, x, x_perm, stage_rows, st->sg));
         MOE_TRY(tm.end(st->sg));
         MOE_HIP(hipEventRecord(ev_g[i], st->sg));
 
@@ -270,11 +298,11 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
         if (dense) {
             if (timing) ++g_timing.dense_stages;
             int64_t r0 = 0;
-            for (int e = 0; e < ef; ++e) r0 += hc[e];
-            for (int e = ef; e < ef + per_stage; ++e) {
-                const int64_t rows = hc[e];
+            for (int b = 0; b < b0; ++b) r0 += hc[b];
+            for (int b = b0; b < b0 + per_stage; ++b) {
+                const int64_t rows = hc[b];
                 if (rows > 0) {
-                    const int64_t wo = (int64_t)e * I * H;
+                    const int64_t wo = (int64_t)(e_w + b - b0) * I * H;
                     MOE_TRY(tm.begin(st->sm, PH_GATEUP));
                     MOE_HIP(launch_dense_gateup(rows, H, I, x_perm + r0 * H, w_gate + wo,
                                                 w_up + wo, act + r0 * I, st->sm));
@@ -293,12 +321,15 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
         } else {
             if (timing) ++g_timing.group_stages;
             if (stage_rows > 0) {
+                // the grouped kernels index weights from their first expert:
+                // shift the offsets so that expert e_w .. is bucket b0 ..
+                const int32_t *goff = off + (b0 - e_w);
                 MOE_TRY(tm.begin(st->sm, PH_GATEUP));
-                MOE_HIP(launch_group_gateup(d, ef, per_stage, off, x_perm, w_gate, w_up, act, grid,
-                                            st->sm));
+                MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, x_perm, w_gate, w_up, act,
+                                            grid, st->sm));
                 MOE_TRY(tm.end(st->sm));
                 MOE_TRY(tm.begin(st->sm, PH_DOWN));
-                MOE_HIP(launch_group_down(d, ef, per_stage, off, act, w_down, y_perm, grid,
+                MOE_HIP(launch_group_down(d, e_w, per_stage, goff, act, w_down, y_perm, grid,
                                           st->sm));
                 MOE_TRY(tm.end(st->sm));
                 if (timing) {
@@ -309,11 +340,13 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
         }
         MOE_HIP(hipEventRecord(ev_m[i], st->sm));
 
-        // weighted combine of this expert group
+        // weighted combine of this stage: its experts over all tokens, or
+        // all experts over its tokens
         MOE_HIP(hipStreamWaitEvent(st->sc, ev_m[i], 0));
         MOE_TRY(tm.begin(st->sc, PH_COMBINE));
-        MOE_HIP(launch_combine(d, ef, per_stage, y_perm, ids, slot_row, wts, y,
-                               (i > 0 || has_shared) ? 1 : 0, st->sc));
+        const int accumulate = (has_shared || (!tok_stages && i > 0)) ? 1 : 0;
+        MOE_HIP(launch_combine(d, tok_stages ? 0 : b0, tok_stages ? EL : per_stage, t_lo, t_hi,
+                               y_perm, ids, slot_row, wts, y, accumulate, st->sc));
         MOE_TRY(tm.end(st->sc));
     }
     MOE_HIP(hipEventRecord(ev_done, st->sc));

@@ -1,16 +1,18 @@
 // Dispatch: histogram, scan, stable scatter and row gather.
 //
-// Order of rows: (local expert ascending, slot ascending); a token selects an
-// expert at most once, so slot order within an expert is token order (the
-// order of the paper's Fig. 7a example).  Three passes, no atomics:
+// Order of rows: (bucket ascending, slot ascending).  A bucket is the local
+// expert, or, when the pipeline cuts token ranges, token-range stage * EL +
+// local expert.  A token selects an expert at most once, so slot order
+// within an expert is token order (the order of the paper's Fig. 7a
+// example).  Three passes, no atomics:
 //   1. one wave per chunk of kPermChunk slots: wave-level match (nine
-//      ballots on the expert id) gives each slot its rank among the equal
+//      ballots on the bucket id) gives each slot its rank among the equal
 //      ids before it in the 64-slot step, a per-chunk LDS counter carries the
-//      rank across steps -> slot_rank, and chunk_counts[chunk][e];
-//   2. one workgroup: per-expert exclusive scan over chunks -> chunk_base,
+//      rank across steps -> slot_rank, and chunk_counts[chunk][b];
+//   2. one workgroup: per-bucket exclusive scan over chunks -> chunk_base,
 //      counts, and a wave-level (DPP row shifts + readlane) scan over
-//      experts -> offsets;
-//   3. one thread per slot: row = offsets[e] + chunk_base[chunk][e] +
+//      buckets -> offsets (and the rows per local expert over stages);
+//   3. one thread per slot: row = offsets[b] + chunk_base[chunk][b] +
 //      slot_rank -> sorted_slot[row], slot_row[slot].
 // The gather copies whole rows with 16-byte loads and stores, one wave per
 // row.
@@ -19,22 +21,28 @@
 namespace moe {
 namespace {
 
+// Bucket of slot s (token s / k) for local expert e, or -1 when not local.
+__device__ __forceinline__ int slot_bucket(const int32_t *ids, int64_t s, int k, int e0, int EL,
+                                           int64_t tps) {
+    int e = ids[s] - e0;
+    if (e < 0 || e >= EL) return -1;
+    if (tps > 0) e += (int)((s / k) / tps) * EL;
+    return e;
+}
+
 __global__ __launch_bounds__(64) void hist_kernel(const int32_t *__restrict__ ids, int64_t nslots,
-                                                  int e0, int EL, int32_t *__restrict__ chunk_counts,
+                                                  int k, int e0, int EL, int64_t tps, int NB,
+                                                  int32_t *__restrict__ chunk_counts,
                                                   int32_t *__restrict__ slot_rank) {
     __shared__ int cnt[kMaxExperts];
     const int lane = threadIdx.x;
-    for (int e = lane; e < EL; e += 64) cnt[e] = 0;
+    for (int e = lane; e < NB; e += 64) cnt[e] = 0;
     __syncthreads();
     const int64_t base = (int64_t)blockIdx.x * kPermChunk;
     const uint64_t lt_mask = (1ull << lane) - 1ull;
     for (int it = 0; it < kPermChunk / 64; ++it) {
         const int64_t s = base + it * 64 + lane;
-        int e = -1;
-        if (s < nslots) {
-            e = ids[s] - e0;
-            if (e < 0 || e >= EL) e = -1;
-        }
+        const int e = s < nslots ? slot_bucket(ids, s, k, e0, EL, tps) : -1;
         // lanes holding the same value (e + 1 in [0, 256], nine bits)
         const uint32_t v = (uint32_t)(e + 1);
         uint64_t match = ~0ull;
@@ -54,7 +62,7 @@ __global__ __launch_bounds__(64) void hist_kernel(const int32_t *__restrict__ id
         if (e >= 0 && before == 0) cnt[e] += __popcll(match);
         __syncthreads();
     }
-    for (int e = lane; e < EL; e += 64) chunk_counts[(int64_t)blockIdx.x * EL + e] = cnt[e];
+    for (int e = lane; e < NB; e += 64) chunk_counts[(int64_t)blockIdx.x * NB + e] = cnt[e];
 }
 
 // Inclusive scan over a wave: DPP row_shr 1, 2, 4, 8 inside each 16-lane row
@@ -74,33 +82,42 @@ __device__ __forceinline__ int wave_inclusive_scan(int v) {
 }
 
 __global__ __launch_bounds__(256) void scan_kernel(const int32_t *__restrict__ chunk_counts,
-                                                   int64_t nchunks, int EL,
+                                                   int64_t nchunks, int NB, int EL,
                                                    int32_t *__restrict__ chunk_base,
                                                    int32_t *__restrict__ counts,
-                                                   int32_t *__restrict__ offsets) {
+                                                   int32_t *__restrict__ offsets,
+                                                   int32_t *__restrict__ counts_el) {
     __shared__ int wave_tot[4];
+    __shared__ int totals[kMaxExperts];
     const int e = threadIdx.x;
     int run = 0;
-    if (e < EL) {
+    if (e < NB) {
         for (int64_t c = 0; c < nchunks; ++c) {
-            const int v = chunk_counts[c * EL + e];
-            chunk_base[c * EL + e] = run;
+            const int v = chunk_counts[c * NB + e];
+            chunk_base[c * NB + e] = run;
             run += v;
         }
         counts[e] = run;
+        totals[e] = run;
     }
-    const int incl = wave_inclusive_scan(e < EL ? run : 0);
+    const int incl = wave_inclusive_scan(e < NB ? run : 0);
     const int w = e >> 6;
     if ((e & 63) == 63) wave_tot[w] = incl;
     __syncthreads();
     int carry = 0;
     for (int i = 0; i < w; ++i) carry += wave_tot[i];
-    if (e < EL) offsets[e] = carry + incl - run;
-    if (e == EL - 1) offsets[EL] = carry + incl;
+    if (e < NB) offsets[e] = carry + incl - run;
+    if (e == NB - 1) offsets[NB] = carry + incl;
+    if (counts_el && e < EL) {  // rows per local expert over the stages
+        int sum = 0;
+        for (int b = e; b < NB; b += EL) sum += totals[b];
+        counts_el[e] = sum;
+    }
 }
 
 __global__ __launch_bounds__(256) void scatter_kernel(const int32_t *__restrict__ ids,
-                                                      int64_t nslots, int e0, int EL,
+                                                      int64_t nslots, int k, int e0, int EL,
+                                                      int64_t tps, int NB,
                                                       const int32_t *__restrict__ chunk_base,
                                                       const int32_t *__restrict__ slot_rank,
                                                       const int32_t *__restrict__ offsets,
@@ -108,13 +125,13 @@ __global__ __launch_bounds__(256) void scatter_kernel(const int32_t *__restrict_
                                                       int32_t *__restrict__ slot_row) {
     const int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (s >= nslots) return;
-    const int e = ids[s] - e0;
-    if (e < 0 || e >= EL) {
+    const int e = slot_bucket(ids, s, k, e0, EL, tps);
+    if (e < 0) {
         slot_row[s] = -1;
         return;
     }
     const int64_t chunk = s / kPermChunk;
-    const int row = offsets[e] + chunk_base[chunk * EL + e] + slot_rank[s];
+    const int row = offsets[e] + chunk_base[chunk * NB + e] + slot_rank[s];
     sorted_slot[row] = (int32_t)s;
     slot_row[s] = row;
 }
@@ -142,20 +159,24 @@ __global__ __launch_bounds__(256) void gather_kernel(const int32_t *__restrict__
 }  // namespace
 
 hipError_t launch_permute(const moe_dims &d, const int32_t *ids, void *ws, const WsLayout &L,
-                          int32_t *counts, int32_t *offsets, int32_t *sorted_slot,
-                          int32_t *slot_row, hipStream_t s) {
+                          int64_t tokens_per_stage, int32_t *counts, int32_t *offsets,
+                          int32_t *counts_el, int32_t *sorted_slot, int32_t *slot_row,
+                          hipStream_t s) {
     char *base = static_cast<char *>(ws);
     int32_t *chunk_counts = reinterpret_cast<int32_t *>(base + L.chunk_counts);
     int32_t *chunk_base = reinterpret_cast<int32_t *>(base + L.chunk_base);
     int32_t *slot_rank = reinterpret_cast<int32_t *>(base + L.slot_rank);
     const int64_t nslots = d.tokens * d.top_k;
-    hist_kernel<<<(unsigned)L.nchunks, 64, 0, s>>>(ids, nslots, d.local_begin, d.local_count,
-                                                    chunk_counts, slot_rank);
-    scan_kernel<<<1, 256, 0, s>>>(chunk_counts, L.nchunks, d.local_count, chunk_base, counts,
-                                  offsets);
+    const int64_t tps = tokens_per_stage;
+    const int NB = L.nbuckets;
+    hist_kernel<<<(unsigned)L.nchunks, 64, 0, s>>>(ids, nslots, d.top_k, d.local_begin,
+                                                    d.local_count, tps, NB, chunk_counts,
+                                                    slot_rank);
+    scan_kernel<<<1, 256, 0, s>>>(chunk_counts, L.nchunks, NB, d.local_count, chunk_base, counts,
+                                  offsets, tps > 0 ? counts_el : nullptr);
     scatter_kernel<<<(unsigned)((nslots + 255) / 256), 256, 0, s>>>(
-        ids, nslots, d.local_begin, d.local_count, chunk_base, slot_rank, offsets, sorted_slot,
-        slot_row);
+        ids, nslots, d.top_k, d.local_begin, d.local_count, tps, NB, chunk_base, slot_rank,
+        offsets, sorted_slot, slot_row);
     return hipGetLastError();
 }
 

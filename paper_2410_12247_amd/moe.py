@@ -17,6 +17,7 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmoe.so")
 
 GEMM_AUTO, GEMM_GROUP, GEMM_DENSE = 0, 1, 2
+CHUNK_EXPERTS, CHUNK_TOKENS = 0, 1
 FLAG_TIMING = 1
 
 # the entry points include/moe.h declares
@@ -42,7 +43,8 @@ class Dims(ctypes.Structure):
 class Opts(ctypes.Structure):
     _fields_ = [("gemm_mode", ctypes.c_int32), ("dense_min_rows", ctypes.c_int32),
                 ("pipeline_n", ctypes.c_int32), ("gemm_cu_budget", ctypes.c_int32),
-                ("flags", ctypes.c_int32), ("reserved", ctypes.c_int32 * 3)]
+                ("flags", ctypes.c_int32), ("chunk_mode", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 2)]
 
 
 class Timing(ctypes.Structure):
@@ -103,10 +105,11 @@ def dims(tokens, hidden, inter, experts, top_k, local_begin=0, local_count=None,
 
 
 def opts(gemm_mode=GEMM_AUTO, dense_min_rows=0, pipeline_n=1, gemm_cu_budget=0,
-         timing=False) -> Opts:
+         timing=False, chunk_mode=CHUNK_EXPERTS) -> Opts:
     o = Opts()
     o.gemm_mode, o.dense_min_rows, o.pipeline_n = gemm_mode, dense_min_rows, pipeline_n
     o.gemm_cu_budget, o.flags = gemm_cu_budget, FLAG_TIMING if timing else 0
+    o.chunk_mode = chunk_mode
     return o
 
 

@@ -87,6 +87,22 @@ def test_invalid_options_and_buffers_rejected():
                                fake, None, None, None, fake, None, None, None, fake, 1 << 40,
                                None)
         assert st == 1, L.moe_last_error()
+    # token-range stages: PN need not divide EL, PN * EL must fit 256 buckets
+    tok = moe.CHUNK_TOKENS
+    assert L.moe_workspace_bytes(ctypes.byref(d), ctypes.byref(moe.opts(pipeline_n=3,
+                                                                        chunk_mode=tok))) > 0
+    assert L.moe_workspace_bytes(ctypes.byref(d), ctypes.byref(moe.opts(pipeline_n=3))) == 0
+    assert L.moe_workspace_bytes(ctypes.byref(d), ctypes.byref(moe.opts(chunk_mode=2))) == 0
+    assert L.moe_workspace_bytes(ctypes.byref(d), ctypes.byref(moe.opts(pipeline_n=33,
+                                                                        chunk_mode=tok))) == 0
+    o = moe.opts(pipeline_n=33, chunk_mode=tok)  # 33 * 8 buckets > 256
+    st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake, fake,
+                           None, None, None, fake, None, None, None, fake, 1 << 40, None)
+    assert st == 2, L.moe_last_error()
+    o = moe.opts(chunk_mode=2)
+    st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake, fake,
+                           None, None, None, fake, None, None, None, fake, 1 << 40, None)
+    assert st == 1
     o = moe.opts()
     o.reserved[1] = 5
     st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake, fake,

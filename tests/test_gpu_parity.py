@@ -200,6 +200,41 @@ def test_forward_invariant_to_pipeline_and_gemm_kind(name):
     assert torch.equal(y, base), "CU budget changes the bits"
 
 
+@pytest.mark.parametrize("name", ["ragged8", "fine", "one"])
+def test_forward_token_range_stages(name):
+    """Token-range stages (each stage all experts over a token range, weights
+    re-read per stage) give the same bits and counts as expert-group stages,
+    for PN that need not divide EL and PN above T."""
+    inp, ids, _ = case(name)
+    g = Dev(inp)
+    s = inp.shape
+    ref = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP))
+    base, counts = ref.y.clone(), ref.counts.clone()
+    for pn in (1, 2, 3, 7):
+        if pn * s.EL > 256:
+            continue
+        for mode in (moe.GEMM_GROUP, moe.GEMM_DENSE, moe.GEMM_AUTO):
+            buf = g.forward(moe.opts(gemm_mode=mode, pipeline_n=pn, chunk_mode=moe.CHUNK_TOKENS))
+            assert torch.equal(buf.y, base), f"token stages PN={pn} mode={mode} differ"
+            assert torch.equal(buf.counts, counts)
+
+
+def test_forward_token_stages_hot_expert_and_empty_stages():
+    """All rows on one expert, PN larger than the token count leaves empty
+    stages; shared experts make every stage accumulate."""
+    shp = C(name="hot_tok", index=208, T=5, H=128, I=64, E=8, EL=8, k=1, renorm=True,
+            n_shared=1, Is=64)
+    inp = synth.make_inputs(shp)
+    inp.bias = np.zeros(8, np.float32)
+    inp.bias[2] = 1e4
+    _, ids, w = oracle.route(inp.x, inp.w_router, inp.bias, 1, True)
+    g = Dev(inp)
+    for pn in (4, 8, 16):
+        buf = g.forward(moe.opts(pipeline_n=pn, chunk_mode=moe.CHUNK_TOKENS))
+        assert np.array_equal(buf.counts.cpu().numpy(), [0, 0, 5, 0, 0, 0, 0, 0])
+        assert_close(buf.y.cpu().numpy(), oracle_y(inp, ids, w, np.arange(5)), f"PN={pn}")
+
+
 def test_forward_all_tokens_to_one_expert():
     shp = C(name="hot", index=206, T=700, H=256, I=128, E=8, EL=8, k=1, renorm=True)
     inp = synth.make_inputs(shp)

@@ -96,27 +96,29 @@ __device__ __forceinline__ float key_logit(uint64_t key) {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// Logits phase layout: 256 threads = 16 token groups x 16 expert groups;
-// a thread owns TT tokens (tg + 16 i: consecutive lanes read rows 36 floats
-// apart, so eight lanes of a 16-byte LDS read land on distinct banks) x TE
-// experts (TE = ceil(E / 16)) and keeps their fma chains in registers.  x
-// and the router are staged through two LDS buffers RT_HC h at a time: the
-// router rows by LDS-DMA, x through registers (widened to fp32), the next
-// chunk in flight while the current one is multiplied; per 4 h a thread
-// reads TT + TE float4 and issues 4*TT*TE fmas.
-constexpr int RT_TG = 16;  // token groups
-constexpr int RT_EG = 16;  // expert groups
-
-// TT tokens per thread, so a workgroup routes 16*TT tokens; the launcher
-// picks TT so that the grid keeps several workgroups per compute unit.
-template <int TE, int TT>
+// Logits phase layout: 256 threads = TG token groups x EG expert groups
+// (EG = 16, or 8 when E <= 8 so that no thread repeats an expert); a thread
+// owns TT tokens (tg + TG i: consecutive lanes read rows 36 floats apart, so
+// eight lanes of a 16-byte LDS read land on distinct banks) x TE experts
+// (TE = ceil(E / EG)) and keeps their fma chains in registers.  x and the
+// router are staged through two LDS buffers RT_HC h at a time: the router
+// rows by LDS-DMA, x through registers (widened to fp32), the next chunk in
+// flight while the current one is multiplied; per 4 h a thread reads
+// TT + TE float4 and issues 4*TT*TE fmas.
+//
+// TT tokens per thread, so a workgroup routes TG*TT <= 64 tokens; the
+// launcher picks TT so that the grid keeps several workgroups per compute
+// unit.
+template <int TE, int TT, int RT_EG>
 __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restrict__ x,
                                                            const float *__restrict__ wr,
                                                            const float *__restrict__ bias,
                                                            int64_t T, int H, int E, int k,
                                                            int renorm, int32_t *__restrict__ ids,
                                                            float *__restrict__ wout) {
-    constexpr int RT_TOK = RT_TG * TT;  // tokens per workgroup
+    constexpr int RT_TG = RT_THREADS / RT_EG;  // token groups
+    constexpr int RT_TOK = RT_TG * TT;          // tokens per workgroup
+    static_assert(RT_TOK <= 64, "x staging covers 64 token rows");
     constexpr int RT_TT = TT;
     constexpr int EMAX = RT_EG * TE;
     constexpr int XS = RT_TOK * RT_LD;  // floats of one x stage
@@ -275,24 +277,27 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
     }
 }
 
-template <int TE, int TT>
+template <int TE, int TT, int EG>
 hipError_t launch_tt(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                      int32_t *ids, float *w, hipStream_t s) {
-    const int64_t blocks = (d.tokens + RT_TG * TT - 1) / (RT_TG * TT);
-    route_kernel<TE, TT><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
+    constexpr int TOK = RT_THREADS / EG * TT;
+    const int64_t blocks = (d.tokens + TOK - 1) / TOK;
+    route_kernel<TE, TT, EG><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
         x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
     return hipGetLastError();
 }
 
-template <int TE>
+template <int TE, int EG = 16>
 hipError_t launch_te(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                      int32_t *ids, float *w, hipStream_t s) {
     // the most tokens per thread (fewest LDS reads per fma) that still
     // leaves enough workgroups per CU to hide latency
+    constexpr int TG = RT_THREADS / EG;
     const int cus = device_cu_count();
-    if (d.tokens >= (int64_t)64 * 4 * cus) return launch_tt<TE, 4>(d, x, wr, bias, ids, w, s);
-    if (d.tokens >= (int64_t)32 * 2 * cus) return launch_tt<TE, 2>(d, x, wr, bias, ids, w, s);
-    return launch_tt<TE, 1>(d, x, wr, bias, ids, w, s);
+    if (TG * 4 <= 64 && d.tokens >= (int64_t)TG * 4 * 4 * cus)
+        return launch_tt<TE, (TG * 4 <= 64 ? 4 : 1), EG>(d, x, wr, bias, ids, w, s);
+    if (d.tokens >= (int64_t)TG * 2 * 2 * cus) return launch_tt<TE, 2, EG>(d, x, wr, bias, ids, w, s);
+    return launch_tt<TE, 1, EG>(d, x, wr, bias, ids, w, s);
 }
 
 }  // namespace
@@ -300,7 +305,8 @@ hipError_t launch_te(const moe_dims &d, const bf16_t *x, const float *wr, const 
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                         int32_t *ids, float *w, hipStream_t s) {
     if (d.tokens <= 0) return hipSuccess;
-    const int te = (d.experts + RT_EG - 1) / RT_EG;
+    if (d.experts <= 8) return launch_te<1, 8>(d, x, wr, bias, ids, w, s);
+    const int te = (d.experts + 15) / 16;
     if (te <= 1) return launch_te<1>(d, x, wr, bias, ids, w, s);
     if (te <= 2) return launch_te<2>(d, x, wr, bias, ids, w, s);
     if (te <= 4) return launch_te<4>(d, x, wr, bias, ids, w, s);

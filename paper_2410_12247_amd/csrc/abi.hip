@@ -199,7 +199,7 @@ moe_status moe_ffn_group(const moe_dims *dims, int32_t e_first, int32_t e_count,
     int grid = cu_budget > 0 ? cu_budget : device_cu_count();
     grid = std::max(8, (grid / 8) * 8);
     hipStream_t s = (hipStream_t)stream;
-    MOE_HIP(launch_group_gateup(*dims, e_first, e_count, offsets, x_perm, w_gate, w_up, act,
+    MOE_HIP(launch_group_gateup(*dims, e_first, e_count, offsets, x_perm, nullptr, w_gate, w_up, act,
                                 grid, s));
     MOE_HIP(launch_group_down(*dims, e_first, e_count, offsets, act, w_down, y_perm, grid, s));
     return MOE_OK;

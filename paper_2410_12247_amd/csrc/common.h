@@ -93,12 +93,14 @@ hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, int64_t t
                           const int32_t *slot_row, const float *w, float *y, int accumulate,
                           hipStream_t s);
 // Grouped GEMMs over local experts [e_first, e_first+e_count) (rows from
-// device offsets).  max_rows bounds the rows of the range (for grid sizing
-// only; pass T*min(k,EL) when unknown).
+// device offsets).  Gate/up takes its token rows either contiguous
+// (row_map NULL: x_rows is x_perm) or straight from the token matrix
+// (x_rows = x, row r is token row_map[r] / top_k, row_map = sorted_slot);
+// the latter needs T*H*2 < 2^32 (byte offsets are 32-bit).
 hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
-                               const int32_t *offsets, const bf16_t *x_perm,
-                               const bf16_t *w_gate, const bf16_t *w_up, bf16_t *act,
-                               int grid, hipStream_t s);
+                               const int32_t *offsets, const bf16_t *x_rows,
+                               const int32_t *row_map, const bf16_t *w_gate,
+                               const bf16_t *w_up, bf16_t *act, int grid, hipStream_t s);
 hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
                              const int32_t *offsets, const bf16_t *act,
                              const bf16_t *w_down, float *y_perm, int grid, hipStream_t s);

@@ -262,6 +262,9 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
         MOE_HIP(hipEventSynchronize(ev_counts));
         hc.assign(st->pinned_counts, st->pinned_counts + NB);
     }
+    // the grouped gate/up GEMM can gather its token rows itself while every
+    // byte offset into x fits 32 bits
+    const bool fold_ok = (uint64_t)T * (uint64_t)H * 2u < (uint64_t(1) << 32);
     int grid = o->gemm_cu_budget > 0 ? o->gemm_cu_budget : device_cu_count();
     grid = std::max(8, (grid / 8) * 8);
 
@@ -287,10 +290,15 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
             }
             if (o->gemm_mode == MOE_GEMM_AUTO) dense = min_rows >= m_star;
         }
-        // gather (dispatch of this stage)
-        MOE_TRY(tm.begin(st->sg, PH_GATHER));
-        MOE_HIP(launch_gather(d, b0, per_stage, off, sorted_slot, x, x_perm, stage_rows, st->sg));
-        MOE_TRY(tm.end(st->sg));
+        // gather (dispatch of this stage); a grouped stage reads its token
+        // rows straight from x through sorted_slot instead
+        const bool fold_gather = !dense && fold_ok;
+        if (!fold_gather) {
+            MOE_TRY(tm.begin(st->sg, PH_GATHER));
+            MOE_HIP(launch_gather(d, b0, per_stage, off, sorted_slot, x, x_perm, stage_rows,
+                                  st->sg));
+            MOE_TRY(tm.end(st->sg));
+        }
         MOE_HIP(hipEventRecord(ev_g[i], st->sg));
 
         // expert GEMMs
@@ -325,8 +333,9 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
                 // shift the offsets so that expert e_w .. is bucket b0 ..
                 const int32_t *goff = off + (b0 - e_w);
                 MOE_TRY(tm.begin(st->sm, PH_GATEUP));
-                MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, x_perm, w_gate, w_up, act,
-                                            grid, st->sm));
+                MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, fold_gather ? x : x_perm,
+                                            fold_gather ? sorted_slot : nullptr, w_gate, w_up,
+                                            act, grid, st->sm));
                 MOE_TRY(tm.end(st->sm));
                 MOE_TRY(tm.begin(st->sm, PH_DOWN));
                 MOE_HIP(launch_group_down(d, e_w, per_stage, goff, act, w_down, y_perm, grid,

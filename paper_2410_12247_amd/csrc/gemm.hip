@@ -79,7 +79,11 @@ struct TileArgs {
     const bf16_t *w0;  // first weight row of the tile (gate rows, or down rows)
     const bf16_t *w1;  // first up row (gate/up only)
     int n_valid;       // weight rows valid from w0 (per half for gate/up)
-    const bf16_t *x;   // first token row of the tile
+    const bf16_t *x;   // first token row of the tile, or the token matrix
+    const int32_t *rows;  // NULL: rows are contiguous from x; else tile row i
+                          // is x row rows[i] / slot_div (the dispatch gather
+                          // folded into the operand loads)
+    int slot_div;
     int m_valid;       // token rows valid from x
     int K;
     void *out;         // output element (first token row, first column)
@@ -150,7 +154,8 @@ __device__ __forceinline__ void run_tile(const TileArgs &a, bf16_t *smem) {
 #pragma unroll
     for (int i = 0; i < C::X_INSTR; ++i) {
         const int r = min(wave * (BM / 4) + i * C::RPI + drow, a.m_valid - 1);
-        xoff[i] = (uint32_t)(r * K + dchunk) * 2u;
+        const int64_t src = a.rows ? (int64_t)(a.rows[r] / a.slot_div) : r;
+        xoff[i] = (uint32_t)((src * K + dchunk) * 2);
     }
     const int w_lds = wave * (BN / 4) * BK;  // element offset of this wave's rows
     const int x_lds = C::STAGE_W + wave * (BM / 4) * BK;
@@ -371,7 +376,8 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
 #pragma unroll
     for (int i = 0; i < C::X_INSTR; ++i) {
         const int r = min(wave * (C::BM / 8) + i * C::RPI + drow, a.m_valid - 1);
-        xoff[i] = (uint32_t)(r * K + dchunk) * 2u;
+        const int64_t src = a.rows ? (int64_t)(a.rows[r] / a.slot_div) : r;
+        xoff[i] = (uint32_t)((src * K + dchunk) * 2);
     }
     const int w_lds = wave * (C::BN / 8) * BK;
     const int x_lds = C::STAGE_W + wave * (C::BM / 8) * BK;
@@ -557,6 +563,8 @@ __global__ __launch_bounds__(TP::THREADS) void dense_kernel(const bf16_t *__rest
     a.w1 = MODE == 0 ? w1 + n0 * K : nullptr;
     a.n_valid = (int)(N - n0);
     a.x = x + m0 * K;
+    a.rows = nullptr;
+    a.slot_div = 1;
     a.m_valid = (int)min<int64_t>(BM, rows - m0);
     a.K = K;
     a.ldo = ldo;
@@ -570,8 +578,8 @@ __global__ __launch_bounds__(TP::THREADS) void dense_kernel(const bf16_t *__rest
 template <int MODE, class TP>
 __global__ __launch_bounds__(TP::THREADS) void group_kernel(
     const int32_t *__restrict__ offsets, int e_first, int e_count, const bf16_t *__restrict__ x,
-    const bf16_t *w0s, const bf16_t *w1s, int64_t wstride, int N, int K, void *out,
-    int64_t ldo) {
+    const int32_t *__restrict__ row_map, int slot_div, const bf16_t *w0s, const bf16_t *w1s,
+    int64_t wstride, int N, int K, void *out, int64_t ldo) {
     constexpr int BM = TP::BM;
     __shared__ __attribute__((aligned(16))) bf16_t smem[TP::LDS_ELEMS];
     __shared__ int s_off[kMaxExperts + 1];
@@ -617,7 +625,9 @@ __global__ __launch_bounds__(TP::THREADS) void group_kernel(
         a.w0 = w0s + woffe + n0 * K;
         a.w1 = MODE == 0 ? w1s + woffe + n0 * K : nullptr;
         a.n_valid = (int)(N - n0);
-        a.x = x + r0 * K;
+        a.x = row_map ? x : x + r0 * K;
+        a.rows = row_map ? row_map + r0 : nullptr;
+        a.slot_div = slot_div;
         a.m_valid = min(BM, cnt - mt * BM);
         a.K = K;
         a.ldo = ldo;
@@ -668,14 +678,14 @@ hipError_t launch_dense_down(int64_t rows, int H, int I, const bf16_t *act,
 }
 
 hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
-                               const int32_t *offsets, const bf16_t *x_perm,
-                               const bf16_t *w_gate, const bf16_t *w_up, bf16_t *act,
-                               int grid, hipStream_t s) {
+                               const int32_t *offsets, const bf16_t *x_rows,
+                               const int32_t *row_map, const bf16_t *w_gate,
+                               const bf16_t *w_up, bf16_t *act, int grid, hipStream_t s) {
     if (e_count <= 0) return hipSuccess;
     using TP = GroupTile<0>;
-    group_kernel<0, TP><<<grid, TP::THREADS, 0, s>>>(offsets, e_first, e_count, x_perm, w_gate,
-                                                     w_up, (int64_t)d.inter * d.hidden, d.inter,
-                                                     d.hidden, act, d.inter);
+    group_kernel<0, TP><<<grid, TP::THREADS, 0, s>>>(
+        offsets, e_first, e_count, x_rows, row_map, d.top_k, w_gate, w_up,
+        (int64_t)d.inter * d.hidden, d.inter, d.hidden, act, d.inter);
     return hipGetLastError();
 }
 
@@ -684,8 +694,8 @@ hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
                              const bf16_t *w_down, float *y_perm, int grid, hipStream_t s) {
     if (e_count <= 0) return hipSuccess;
     using TP = GroupTile<1>;
-    group_kernel<1, TP><<<grid, TP::THREADS, 0, s>>>(offsets, e_first, e_count, act, w_down,
-                                                     nullptr, (int64_t)d.hidden * d.inter,
+    group_kernel<1, TP><<<grid, TP::THREADS, 0, s>>>(offsets, e_first, e_count, act, nullptr, 1,
+                                                     w_down, nullptr, (int64_t)d.hidden * d.inter,
                                                      d.hidden, d.inter, y_perm, d.hidden);
     return hipGetLastError();
 }

@@ -7,11 +7,22 @@
 //
 // One wave per token: the wave reads the token's k slot records, orders the
 // selected ones by expert id (each ranked by counting smaller ids), then streams
-// the hidden dimension in 16-byte vectors.
+// the hidden dimension in 16-byte vectors, four per lane per pass so that all
+// loads of a pass are in flight together.
 #include "common.h"
 
 namespace moe {
 namespace {
+
+// y_perm rows and y are each touched once: streaming (nontemporal) access
+// keeps them from evicting reusable lines from the caches
+__device__ __forceinline__ float4 load_stream(const float4 *p) {
+    return __builtin_bit_cast(float4,
+                              __builtin_nontemporal_load(reinterpret_cast<const floatx4 *>(p)));
+}
+__device__ __forceinline__ void store_stream(float4 *p, float4 v) {
+    __builtin_nontemporal_store(__builtin_bit_cast(floatx4, v), reinterpret_cast<floatx4 *>(p));
+}
 
 __global__ __launch_bounds__(256) void combine_kernel(int64_t t_begin, int64_t t_end, int H,
                                                       int k, int e0,
@@ -71,23 +82,37 @@ __global__ __launch_bounds__(256) void combine_kernel(int64_t t_begin, int64_t t
         ++n;
     }
     if (n == 0 && accumulate) return;
-    const int vecs = H / 4;
+    const int vecs = H / 4;  // H is a multiple of 64: vecs is a multiple of 16
     float4 *yrow = reinterpret_cast<float4 *>(y + t * H);
-    for (int v = lane; v < vecs; v += 64) {
-        float4 acc = accumulate ? yrow[v] : make_float4(0.f, 0.f, 0.f, 0.f);
+    // four 16-byte vectors per lane per pass: all loads of a pass in flight
+    for (int v0 = lane; v0 < vecs; v0 += 256) {
+        float4 acc[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int v = min(v0 + 64 * u, vecs - 1);
+            acc[u] = accumulate ? load_stream(yrow + v) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
 #pragma unroll
         for (int j = 0; j < kMaxTopK; ++j) {
             if (j < n) {
-                const float4 p =
-                    reinterpret_cast<const float4 *>(y_perm + (int64_t)orow[j] * H)[v];
+                const float4 *prow =
+                    reinterpret_cast<const float4 *>(y_perm + (int64_t)orow[j] * H);
                 const float c = ow[j];
-                acc.x = __builtin_fmaf(c, p.x, acc.x);
-                acc.y = __builtin_fmaf(c, p.y, acc.y);
-                acc.z = __builtin_fmaf(c, p.z, acc.z);
-                acc.w = __builtin_fmaf(c, p.w, acc.w);
+                float4 p[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) p[u] = load_stream(prow + min(v0 + 64 * u, vecs - 1));
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    acc[u].x = __builtin_fmaf(c, p[u].x, acc[u].x);
+                    acc[u].y = __builtin_fmaf(c, p[u].y, acc[u].y);
+                    acc[u].z = __builtin_fmaf(c, p[u].z, acc[u].z);
+                    acc[u].w = __builtin_fmaf(c, p[u].w, acc[u].w);
+                }
             }
         }
-        yrow[v] = acc;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (v0 + 64 * u < vecs) store_stream(yrow + v0 + 64 * u, acc[u]);
     }
 }
 

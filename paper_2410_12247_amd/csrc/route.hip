@@ -20,8 +20,6 @@ namespace {
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
 
-constexpr int RT_HC = 32;   // h per LDS chunk
-constexpr int RT_LD = RT_HC + 4;
 constexpr int RT_THREADS = 256;
 
 template <int CTRL>
@@ -101,15 +99,17 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 // owns TT tokens (tg + TG i: consecutive lanes read rows 36 floats apart, so
 // eight lanes of a 16-byte LDS read land on distinct banks) x TE experts
 // (TE = ceil(E / EG)) and keeps their fma chains in registers.  x and the
-// router are staged through two LDS buffers RT_HC h at a time: the router
-// rows by LDS-DMA, x through registers (widened to fp32), the next chunk in
+// router are staged through two LDS buffers HC h at a time: the router rows
+// by LDS-DMA, x through registers (widened to fp32), the next chunk in
 // flight while the current one is multiplied; per 4 h a thread reads
-// TT + TE float4 and issues 4*TT*TE fmas.
+// TT + TE float4 and issues 4*TT*TE fmas.  With few experts the fmas per
+// chunk are few, so the chunk is longer (HC = 128) to keep more bytes in
+// flight per wait.
 //
 // TT tokens per thread, so a workgroup routes TG*TT <= 64 tokens; the
 // launcher picks TT so that the grid keeps several workgroups per compute
 // unit.
-template <int TE, int TT, int RT_EG>
+template <int TE, int TT, int RT_EG, int HC>
 __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restrict__ x,
                                                            const float *__restrict__ wr,
                                                            const float *__restrict__ bias,
@@ -118,11 +118,14 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
                                                            float *__restrict__ wout) {
     constexpr int RT_TG = RT_THREADS / RT_EG;  // token groups
     constexpr int RT_TOK = RT_TG * TT;          // tokens per workgroup
-    static_assert(RT_TOK <= 64, "x staging covers 64 token rows");
+    static_assert(RT_TOK <= 64, "a workgroup routes at most 64 tokens");
+    static_assert(HC % 32 == 0, "router rows are staged in 128-byte segments");
     constexpr int RT_TT = TT;
+    constexpr int RT_HC = HC;
+    constexpr int RT_LD = HC + 4;       // x row stride in LDS (floats)
     constexpr int EMAX = RT_EG * TE;
     constexpr int XS = RT_TOK * RT_LD;  // floats of one x stage
-    constexpr int WS = EMAX * RT_HC;    // floats of one router stage (128-byte rows)
+    constexpr int WS = EMAX * RT_HC;    // floats of one router stage
     constexpr int P1 = 2 * XS + 2 * WS;
     constexpr int P2 = RT_TOK * (EMAX + 1);  // selection phase
     __shared__ __attribute__((aligned(16))) float lds[P1 > P2 ? P1 : P2];
@@ -140,41 +143,60 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
 #pragma unroll
         for (int j = 0; j < TE; ++j) acc[i][j] = 0.0f;
 
-    // x: one 16-byte (8 bf16) piece per thread, widened to fp32 in LDS
-    const int xtok = (tid >> 2) % RT_TOK, xpart = tid & 3;  // threads past 4*TB repeat rows
-    const int64_t xt = min<int64_t>(t0 + xtok, T - 1);
-    const bf16_t *xrow = x + xt * H + xpart * 8;
-    // router: LDS-DMA of 8 rows x 128 bytes per wave-wide instruction;
-    // 16-byte chunk c of row r sits at chunk c ^ (r & 7)
-    const int n_wdma = (E + 7) / 8;
+    // x: 16-byte (8 bf16) pieces, PPT per thread, widened to fp32 in LDS;
+    // piece p covers token row p / PPR, h 8 * (p % PPR) of the chunk
+    constexpr int PPR = HC / 8;
+    constexpr int NPIECE = RT_TOK * PPR;
+    constexpr int PPT = (NPIECE + RT_THREADS - 1) / RT_THREADS;
+    const bf16_t *xsrc[PPT];
+    int xdst[PPT];
+#pragma unroll
+    for (int q = 0; q < PPT; ++q) {
+        const int pc = min(tid + RT_THREADS * q, NPIECE - 1);  // repeats write equal values
+        const int64_t xt = min<int64_t>(t0 + pc / PPR, T - 1);
+        xsrc[q] = x + xt * H + (pc % PPR) * 8;
+        xdst[q] = (pc / PPR) * RT_LD + (pc % PPR) * 8;
+    }
+    // router: LDS-DMA of 8 rows x one 128-byte segment per wave-wide
+    // instruction; stage layout [row block of 8][segment][8 rows][32 floats],
+    // 16-byte chunk c of a row's segment at chunk c ^ (row & 7)
+    constexpr int NSEG = HC / 32;
+    const int n_wdma = (E + 7) / 8 * NSEG;
     const int drow = lane >> 3;
     const int dchunk = (lane & 7) ^ (drow & 7);
     auto issue_w = [&](int h0, float *wsb) {
         for (int q = wave; q < n_wdma; q += RT_THREADS / 64) {
-            const int r = min(q * 8 + drow, E - 1);  // rows past E: a copy, never read
+            const int blk = q / NSEG, seg = q % NSEG;
+            const int r = min(blk * 8 + drow, E - 1);  // rows past E: a copy, never read
             __builtin_amdgcn_global_load_lds(
-                (gbl_void_t *)(wr + (int64_t)r * H + h0 + dchunk * 4),
-                (lds_void_t *)(wsb + q * 8 * RT_HC), 16, 0, 0);
+                (gbl_void_t *)(wr + (int64_t)r * H + h0 + seg * 32 + dchunk * 4),
+                (lds_void_t *)(wsb + blk * 8 * HC + seg * 256), 16, 0, 0);
         }
     };
 
-    uint4 xr = *reinterpret_cast<const uint4 *>(xrow);
+    uint4 xr[PPT];
+#pragma unroll
+    for (int q = 0; q < PPT; ++q) xr[q] = *reinterpret_cast<const uint4 *>(xsrc[q]);
     issue_w(0, lds + 2 * XS);
     const int nchunk = H / RT_HC;
     for (int c = 0; c < nchunk; ++c) {
         const int st = c & 1;
         float *xs = lds + st * XS;
         const float *ws = lds + 2 * XS + st * WS;
-        {
-            const float4 a = make_float4(bf16_lo(xr.x), bf16_hi(xr.x), bf16_lo(xr.y), bf16_hi(xr.y));
-            const float4 b = make_float4(bf16_lo(xr.z), bf16_hi(xr.z), bf16_lo(xr.w), bf16_hi(xr.w));
-            *reinterpret_cast<float4 *>(xs + xtok * RT_LD + xpart * 8) = a;
-            *reinterpret_cast<float4 *>(xs + xtok * RT_LD + xpart * 8 + 4) = b;
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const uint4 v = xr[q];
+            const float4 a = make_float4(bf16_lo(v.x), bf16_hi(v.x), bf16_lo(v.y), bf16_hi(v.y));
+            const float4 b = make_float4(bf16_lo(v.z), bf16_hi(v.z), bf16_lo(v.w), bf16_hi(v.w));
+            *reinterpret_cast<float4 *>(xs + xdst[q]) = a;
+            *reinterpret_cast<float4 *>(xs + xdst[q] + 4) = b;
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this chunk's router rows landed
         __syncthreads();  // ... for every wave; chunk c-1 fully consumed
         if (c + 1 < nchunk) {
-            xr = *reinterpret_cast<const uint4 *>(xrow + (c + 1) * RT_HC);
+#pragma unroll
+            for (int q = 0; q < PPT; ++q)
+                xr[q] = *reinterpret_cast<const uint4 *>(xsrc[q] + (c + 1) * RT_HC);
             issue_w((c + 1) * RT_HC, lds + 2 * XS + (st ^ 1) * WS);
         }
 #pragma unroll
@@ -187,8 +209,9 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
 #pragma unroll
             for (int j = 0; j < TE; ++j) {
                 const int e = min(eg * TE + j, EMAX - 1);
-                wv[j] = *reinterpret_cast<const float4 *>(ws + e * RT_HC +
-                                                          (((hh >> 2) ^ (e & 7)) << 2));
+                wv[j] = *reinterpret_cast<const float4 *>(
+                    ws + (e >> 3) * 8 * HC + (hh >> 5) * 256 + (e & 7) * 32 +
+                    ((((hh >> 2) & 7) ^ (e & 7)) << 2));
             }
 #pragma unroll
             for (int j = 0; j < TE; ++j) {
@@ -282,8 +305,19 @@ hipError_t launch_tt(const moe_dims &d, const bf16_t *x, const float *wr, const 
                      int32_t *ids, float *w, hipStream_t s) {
     constexpr int TOK = RT_THREADS / EG * TT;
     const int64_t blocks = (d.tokens + TOK - 1) / TOK;
-    route_kernel<TE, TT, EG><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
-        x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
+    // longer chunks when few experts give little work per chunk (H is a
+    // multiple of 64; 128-h chunks need a multiple of 128)
+    if constexpr (TE == 1) {
+        if (d.hidden % 128 == 0)
+            route_kernel<TE, TT, EG, 128><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
+                x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
+        else
+            route_kernel<TE, TT, EG, 64><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
+                x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
+    } else {
+        route_kernel<TE, TT, EG, 32><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
+            x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
+    }
     return hipGetLastError();
 }
 

@@ -28,6 +28,8 @@
 // Both map workgroups to tiles XCD by XCD (the hardware deals workgroups
 // round-robin over the 8 XCDs), so the tiles running on one XCD are
 // neighbours in (m, n) and share activation and weight rows in its L2.
+#include <type_traits>
+
 #include "common.h"
 
 namespace moe {
@@ -348,6 +350,11 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
     const int wm = wave >> 1;   // 64-row token block
     const int K = a.K;
     const int nk = K / BK;
+    // a wave whose token rows or weight rows all lie past the valid edge of
+    // a partial tile skips its MFMAs (its outputs are never stored); it still
+    // takes its share of the loads and barriers
+    const bool active = wm * C::WTM < a.m_valid &&
+                        (MODE == 0 ? wn * (C::WTN / 2) : wn * C::WTN) < a.n_valid;
 
     floatx4 acc[C::TN][C::TM];
 #pragma unroll
@@ -437,13 +444,15 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
     wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
 
-    if (grp == 0) {
+    // the two groups' loops, with or without the MFMAs; each is straight
+    // code (no branch around the MFMA block inside the loop)
+    auto loop_a = [&](auto with_mfma) {
         load_frags(0);
         for (int k = 0; k < nk; ++k) {
             // compute phase: stage k
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             __builtin_amdgcn_s_setprio(1);
-            mfmas();
+            if constexpr (decltype(with_mfma)::value) mfmas();
             __builtin_amdgcn_s_setprio(0);
             // stage k+1 (requested two iterations ago) landed before the barrier
             wait_vmcnt<C::LPS>();
@@ -453,7 +462,8 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
             issue(k + NS - 1);
             __builtin_amdgcn_s_barrier();
         }
-    } else {
+    };
+    auto loop_b = [&](auto with_mfma) {
         for (int k = 0; k < nk; ++k) {
             // memory phase: fragments of stage k, this wave's share of stage k+3
             load_frags(k);
@@ -465,10 +475,17 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
             // compute phase: stage k
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             __builtin_amdgcn_s_setprio(1);
-            mfmas();
+            if constexpr (decltype(with_mfma)::value) mfmas();
             __builtin_amdgcn_s_setprio(0);
             __builtin_amdgcn_s_barrier();
         }
+    };
+    using on = std::integral_constant<bool, true>;
+    using off = std::integral_constant<bool, false>;
+    if (grp == 0) {
+        if (active) loop_a(on{}); else loop_a(off{});
+    } else {
+        if (active) loop_b(on{}); else loop_b(off{});
     }
     wait_vmcnt<0>();  // clamped tail requests drained before LDS is reused
     __builtin_amdgcn_s_barrier();

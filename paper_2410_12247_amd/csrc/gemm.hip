@@ -310,37 +310,47 @@ __device__ __forceinline__ void run_tile(const TileArgs &a, bf16_t *smem) {
 }
 
 // ---------------------------------------------------------------------------
-// Eight-wave ping-pong variant.  256 x 256 output tile, eight waves in two
-// groups of four, one wave of each group on every SIMD.  Each wave owns a
-// 128 (weights) x 64 (tokens) accumulator block (128 AGPRs).  The groups
-// alternate between a compute phase (32 MFMAs on fragments already in
-// registers) and a memory phase (its share of the LDS-DMA for stage k+3 and
-// the 12 fragment reads of its next stage), separated by workgroup
-// barriers, so every SIMD always has one wave issuing MFMAs while the other
-// feeds LDS.  Stage s lives in LDS buffer s % 4.
-//   group A (waves 0-3, token rows   0..127): compute(k) | mem: frags(k+1), DMA(k+3)
-//   group B (waves 4-7, token rows 128..255): mem: frags(k), DMA(k+3) | compute(k)
+// Eight-wave ping-pong variant.  256 (weights) x BM (tokens) output tile,
+// eight waves in two groups of four, one wave of each group on every SIMD.
+// Each wave owns a 128 x BM/4 accumulator block.  The groups alternate
+// between a compute phase (MFMAs on fragments already in registers) and a
+// memory phase (its share of the LDS-DMA for stage k+3 and the fragment
+// reads of its next stage), separated by workgroup barriers, so every SIMD
+// always has one wave issuing MFMAs while the other feeds LDS.  Stage s
+// lives in LDS buffer s % 4.
+//   group A (waves 0-3, token rows 0..BM/2-1):  compute(k) | mem: frags(k+1), DMA(k+3)
+//   group B (waves 4-7, token rows BM/2..BM-1): mem: frags(k), DMA(k+3) | compute(k)
+// LDS traffic per MFMA falls as the wave tile grows: BM = 320 (wave tile
+// 128 x 80, 40 MFMAs per 13 fragment reads, 160 accumulator registers, four
+// 36 KiB stages) is the largest that fits 256 registers and 160 KiB of LDS.
 // ---------------------------------------------------------------------------
 constexpr int PP_THREADS = 512;
 
-template <int MODE>
+template <int MODE, int BM_>
 struct PPCfg {
-    static constexpr int BN = 256, BM = 256, BK = 32, NS = 4;
-    static constexpr int WTN = 128, WTM = 64;  // wave tile (weights x tokens)
+    static constexpr int BN = 256, BM = BM_, BK = 32, NS = 4;
+    static constexpr int WTN = 128, WTM = BM / 4;  // wave tile (weights x tokens)
     static constexpr int TN = WTN / 16, TM = WTM / 16;
+    static_assert(WTM % 16 == 0, "token rows per wave: whole 16-row fragments");
     static constexpr int CPR = BK / 8;          // 16-byte chunks per LDS row
     static constexpr int RPI = 64 / CPR;        // rows one LDS-DMA instruction fills
     static constexpr int W_INSTR = BN / 8 / RPI;
-    static constexpr int X_INSTR = BM / 8 / RPI;
-    static constexpr int LPS = W_INSTR + X_INSTR;  // DMA instructions per wave per stage
+    // token rows: BM / RPI instructions, group A's waves take X_INSTR_A
+    // each, group B's the rest
+    static constexpr int X_TOTAL = BM / RPI;
+    static constexpr int X_INSTR_A = (X_TOTAL + 7) / 8;
+    static constexpr int X_INSTR_B = (X_TOTAL - 4 * X_INSTR_A) / 4;
+    static_assert(4 * X_INSTR_A + 4 * X_INSTR_B == X_TOTAL, "token rows split over waves");
+    static constexpr int LPS_A = W_INSTR + X_INSTR_A;  // DMA instructions per wave per stage
+    static constexpr int LPS_B = W_INSTR + X_INSTR_B;
     static constexpr int STAGE_W = BN * BK, STAGE_X = BM * BK, STAGE = STAGE_W + STAGE_X;
     static constexpr int LDS_ELEMS = NS * STAGE;
     static constexpr int BNOUT = MODE == 0 ? BN / 2 : BN;
 };
 
-template <int MODE>
+template <int MODE, int BM_>
 __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
-    using C = PPCfg<MODE>;
+    using C = PPCfg<MODE, BM_>;
     constexpr int BK = C::BK, NS = C::NS;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -362,7 +372,9 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
 #pragma unroll
         for (int m = 0; m < C::TM; ++m) acc[t][m] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    // ---- LDS-DMA share of this wave: 32 weight rows and 32 token rows
+    // ---- LDS-DMA share of this wave: BN/8 weight rows and a slice of the
+    // token rows (BM/16 instructions of 16 rows split over the waves,
+    // group A's waves taking the larger slices when they do not divide evenly)
     const int drow = lane / C::CPR;
     const int dchunk = ((lane % C::CPR) ^ swz<BK>(drow)) * 8;
     const bf16_t *wsrc;
@@ -374,21 +386,26 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
         wsrc = a.w0;
         wrow0 = wave * (C::BN / 8);
     }
-    uint32_t woff[C::W_INSTR], xoff[C::X_INSTR];
+    uint32_t woff[C::W_INSTR], xoff[C::X_INSTR_A];
 #pragma unroll
     for (int i = 0; i < C::W_INSTR; ++i) {
         const int r = min(wrow0 + i * C::RPI + drow, a.n_valid - 1);
         woff[i] = (uint32_t)(r * K + dchunk) * 2u;
     }
+    // first token row of this wave's LDS-DMA share
+    const int x_row0 = grp == 0 ? wave * C::X_INSTR_A * C::RPI
+                                : 4 * C::X_INSTR_A * C::RPI + (wave - 4) * C::X_INSTR_B * C::RPI;
 #pragma unroll
-    for (int i = 0; i < C::X_INSTR; ++i) {
-        const int r = min(wave * (C::BM / 8) + i * C::RPI + drow, a.m_valid - 1);
+    for (int i = 0; i < C::X_INSTR_A; ++i) {
+        const int r = min(x_row0 + i * C::RPI + drow, a.m_valid - 1);
         const int64_t src = a.rows ? (int64_t)(a.rows[r] / a.slot_div) : r;
         xoff[i] = (uint32_t)((src * K + dchunk) * 2);
     }
     const int w_lds = wave * (C::BN / 8) * BK;
-    const int x_lds = C::STAGE_W + wave * (C::BM / 8) * BK;
-    auto issue = [&](int kstage) {  // this wave's share of stage kstage (clamped)
+    const int x_lds = C::STAGE_W + x_row0 * BK;
+    // this wave's share of stage kstage (clamped); nx: its token-row
+    // instruction count (the group's)
+    auto issue = [&](int kstage, auto nx) {
         const int ks = min(kstage, nk - 1);
         bf16_t *sb = smem + (kstage % NS) * C::STAGE;
         const char *wk = reinterpret_cast<const char *>(wsrc + ks * BK);
@@ -399,7 +416,7 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
                                              (lds_void_t *)(sb + w_lds + i * C::RPI * BK), 16,
                                              0, 0);
 #pragma unroll
-        for (int i = 0; i < C::X_INSTR; ++i)
+        for (int i = 0; i < decltype(nx)::value; ++i)
             __builtin_amdgcn_global_load_lds((gbl_void_t *)(xk + xoff[i]),
                                              (lds_void_t *)(sb + x_lds + i * C::RPI * BK), 16,
                                              0, 0);
@@ -439,8 +456,12 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
     };
 
     // prologue: stages 0..2 requested by every wave, all landed
+    using nxa = std::integral_constant<int, C::X_INSTR_A>;
+    using nxb = std::integral_constant<int, C::X_INSTR_B>;
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s) issue(s);
+    for (int s = 0; s < NS - 1; ++s) {
+        if (grp == 0) issue(s, nxa{}); else issue(s, nxb{});
+    }
     wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
 
@@ -455,11 +476,11 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
             if constexpr (decltype(with_mfma)::value) mfmas();
             __builtin_amdgcn_s_setprio(0);
             // stage k+1 (requested two iterations ago) landed before the barrier
-            wait_vmcnt<C::LPS>();
+            wait_vmcnt<C::LPS_A>();
             __builtin_amdgcn_s_barrier();
             // memory phase: fragments of stage k+1, this wave's share of stage k+3
             load_frags(k + 1);
-            issue(k + NS - 1);
+            issue(k + NS - 1, nxa{});
             __builtin_amdgcn_s_barrier();
         }
     };
@@ -467,10 +488,10 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
         for (int k = 0; k < nk; ++k) {
             // memory phase: fragments of stage k, this wave's share of stage k+3
             load_frags(k);
-            issue(k + NS - 1);
+            issue(k + NS - 1, nxb{});
             // stage k+1 (requested in iteration k-2) landed; the requests of
             // iterations k-1 and k may stay in flight
-            wait_vmcnt<2 * C::LPS>();
+            wait_vmcnt<2 * C::LPS_B>();
             __builtin_amdgcn_s_barrier();
             // compute phase: stage k
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -548,15 +569,15 @@ struct FourWave {
         run_tile<MODE, BN_, BM_, BK, NS>(a, smem);
     }
 };
-template <int MODE>
+template <int MODE, int BM_>
 struct PingPong {
-    using C = PPCfg<MODE>;
+    using C = PPCfg<MODE, BM_>;
     static constexpr int THREADS = PP_THREADS;
     static constexpr int BM = C::BM;
     static constexpr int BNOUT = C::BNOUT;
     static constexpr int LDS_ELEMS = C::LDS_ELEMS;
     static __device__ __forceinline__ void run(const TileArgs &a, bf16_t *smem) {
-        run_tile_pp<MODE>(a, smem);
+        run_tile_pp<MODE, BM_>(a, smem);
     }
 };
 
@@ -661,8 +682,9 @@ __global__ __launch_bounds__(TP::THREADS) void group_kernel(
 #define MOE_GEMM_PINGPONG 1
 #endif
 #if MOE_GEMM_PINGPONG
-template <int MODE> using DenseTile = PingPong<MODE>;
-template <int MODE> using GroupTile = PingPong<MODE>;
+constexpr int kTokenTile = 320;
+template <int MODE> using DenseTile = PingPong<MODE, kTokenTile>;
+template <int MODE> using GroupTile = PingPong<MODE, kTokenTile>;
 #else
 template <int MODE> using DenseTile = FourWave<MODE, 256, 256, 32, 4>;
 template <int MODE> using GroupTile = FourWave<MODE, 256, 256, 32, 4>;

@@ -29,6 +29,9 @@ CASES = {
     "k_eq_E": C(name="k_eq_E", index=204, T=64, H=128, I=64, E=6, EL=6, k=6, renorm=False),
     # a single token
     "one": C(name="one", index=205, T=1, H=256, I=256, E=8, EL=8, k=2, renorm=True),
+    # few experts with many rows each: several grouped token tiles per expert
+    # plus a ragged last one
+    "tall4": C(name="tall4", index=209, T=1500, H=192, I=320, E=4, EL=4, k=2, renorm=True),
 }
 
 _cache = {}

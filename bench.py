@@ -26,6 +26,7 @@ if ROOT not in sys.path:
 
 METRIC = "MoE FFN prefill tokens/sec on 1 MI355X; expert-GEMM % of bf16 MFMA peak"
 PEAK_BF16_FLOPS = 2.5e15   # MI355X dense bf16 MFMA, published
+PHASE_STEPS = 5            # steps with every phase timed, for the breakdown
 PEAK_HBM_BYTES = 8.0e12    # MI355X HBM3E, published
 
 WORKLOAD_TEXT = {
@@ -209,8 +210,15 @@ def main(argv=None):
     if args.tokens:
         shape = shape.with_tokens(args.tokens)
     inp = synth.make_inputs(shape)
-    wall, tms, counts = run_workload(args, shape, inp, args.steps, args.warmup)
+    # timed steps: events around the GEMM launches only (an event between two
+    # kernels delays the second); then a few steps with every phase timed
+    # for the breakdown of the other phases
+    wall, tms, counts = run_workload(args, shape, inp, args.steps, args.warmup, timing="gemm")
     tm = summarize_timing(tms)
+    _, tms_all, _ = run_workload(args, shape, inp, PHASE_STEPS, 1, timing=True)
+    tm_all = summarize_timing(tms_all)
+    for k in ("route_ms", "permute_ms", "gather_ms", "combine_ms", "total_ms"):
+        tm[k] = tm_all[k]
     R = int(counts.sum())
     fg, fd, fs = gemm_flops(shape, R)
     ms = wall / args.steps * 1e3
@@ -288,7 +296,8 @@ def sweep(args):
         res = {}
         for mode in ("group", "dense", "auto"):
             a = argparse.Namespace(**{**vars(args), "mode": mode})
-            wall, tms, counts = run_workload(a, shape, inp, args.steps, args.warmup)
+            wall, tms, counts = run_workload(a, shape, inp, args.steps, args.warmup,
+                                             timing="gemm")
             tm = summarize_timing(tms)
             res[mode] = {"ms": round(wall / args.steps * 1e3, 4),
                          "gemm_ms": round(tm["gateup_ms"] + tm["down_ms"], 4),

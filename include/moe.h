@@ -66,7 +66,7 @@ typedef struct {
 
 enum { MOE_GEMM_AUTO = 0, MOE_GEMM_GROUP = 1, MOE_GEMM_DENSE = 2 };
 enum { MOE_CHUNK_EXPERTS = 0, MOE_CHUNK_TOKENS = 1 };
-enum { MOE_FLAG_TIMING = 1 };
+enum { MOE_FLAG_TIMING = 1, MOE_FLAG_TIMING_GEMM = 2 };
 
 /* Options of moe_ffn_forward (Sec. 4.3 of the paper: the GroupGemm /
  * DenseGemm switch by load, the pipeline number PN and how the work is cut
@@ -90,13 +90,21 @@ typedef struct {
     int32_t gemm_cu_budget; /* workgroups of the persistent grouped GEMM;
                                0 = one per compute unit */
     int32_t flags;          /* MOE_FLAG_TIMING: time each phase with HIP
-                               events (read with moe_last_timing) */
+                               events (read with moe_last_timing).
+                               MOE_FLAG_TIMING_GEMM: time only the expert
+                               GEMM launches (gate/up, down, shared), with
+                               one event between consecutive launches of a
+                               stream; the other phases read 0.  Every
+                               event recorded between two kernels delays
+                               the second, so this is the mode to time a
+                               run whose wall time also matters. */
     int32_t chunk_mode;     /* MOE_CHUNK_EXPERTS or MOE_CHUNK_TOKENS */
     int32_t reserved[2];    /* must be zero */
 } moe_opts;
 
 /* Per-phase device time of the last moe_ffn_forward call on this thread
- * that had MOE_FLAG_TIMING set, in milliseconds, summed over stages. */
+ * that had MOE_FLAG_TIMING or MOE_FLAG_TIMING_GEMM set, in milliseconds,
+ * summed over stages. */
 typedef struct {
     float route_ms, permute_ms, gather_ms, gateup_ms, down_ms, shared_ms,
         combine_ms, total_ms;

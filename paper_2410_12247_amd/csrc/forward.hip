@@ -88,41 +88,63 @@ struct TimingRecord {
 };
 thread_local TimingRecord g_timing;
 
-// Records spans into the calling thread's record when enabled.
+// Records spans into the calling thread's record when enabled: every
+// phase (MOE_FLAG_TIMING), or only the GEMM phases (MOE_FLAG_TIMING_GEMM).
+// A span that starts on the stream where the previous span just ended, with
+// nothing enqueued in between, reuses that span's stop event as its start.
 class Timer {
    public:
-    Timer(DevState *st, bool on) : st_(st), on_(on) {}
+    Timer(DevState *st, int flags)
+        : st_(st), all_((flags & MOE_FLAG_TIMING) != 0),
+          gemm_((flags & (MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM)) != 0) {}
     // Starts a span of `phase` on stream s; returns its index (or -1).
     moe_status begin(hipStream_t s, int phase, int *idx = nullptr) {
         int &i = idx ? *idx : cur_;
         i = -1;
-        if (!on_) return MOE_OK;
+        if (!timed(phase)) {
+            chain_ = false;
+            return MOE_OK;
+        }
         hipEvent_t a, b;
+        // (the caller's stream may be the null stream: compare only after a
+        // span has ended)
+        const bool chain = chain_ && last_s_ == s;
         {
             std::lock_guard<std::mutex> lock(g_mu);
             MOE_TRY(ensure_events(st_->time_ev, used_ + 2, hipEventDefault));
-            a = st_->time_ev[used_];
+            a = chain ? last_stop_ : st_->time_ev[used_];
             b = st_->time_ev[used_ + 1];
         }
         used_ += 2;
-        MOE_HIP(hipEventRecord(a, s));
+        if (!chain) MOE_HIP(hipEventRecord(a, s));
+        chain_ = false;
         i = (int)g_timing.spans.size();
         g_timing.spans.push_back({phase, a, b});
         return MOE_OK;
     }
     moe_status end(hipStream_t s, int idx = -2) {
-        if (!on_) return MOE_OK;
         const int i = idx == -2 ? cur_ : idx;
         if (i < 0) return MOE_OK;
         MOE_HIP(hipEventRecord(g_timing.spans[i].stop, s));
+        chain_ = true;
+        last_s_ = s;
+        last_stop_ = g_timing.spans[i].stop;
         return MOE_OK;
     }
+    // Something else was enqueued: the next span records its own start.
+    void gap() { chain_ = false; }
 
    private:
+    bool timed(int phase) const {
+        return all_ || (gemm_ && (phase == PH_GATEUP || phase == PH_DOWN || phase == PH_SHARED));
+    }
     DevState *st_;
-    bool on_;
+    bool all_, gemm_;
     size_t used_ = 0;
     int cur_ = -1;
+    bool chain_ = false;  // the last enqueue was a span's stop event
+    hipStream_t last_s_ = nullptr;
+    hipEvent_t last_stop_ = nullptr;
 };
 
 moe_status check_opts(const moe_dims *d, const moe_opts *o) {
@@ -140,7 +162,8 @@ moe_status check_opts(const moe_dims *d, const moe_opts *o) {
         return fail(MOE_ERR_UNSUPPORTED, "token stages: pipeline_n * local_count > %d",
                     kMaxExperts);
     if (o->gemm_cu_budget < 0) return fail(MOE_ERR_INVALID, "gemm_cu_budget < 0");
-    if (o->flags & ~MOE_FLAG_TIMING) return fail(MOE_ERR_INVALID, "unknown flags 0x%x", o->flags);
+    if (o->flags & ~(MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM))
+        return fail(MOE_ERR_INVALID, "unknown flags 0x%x", o->flags);
     for (int i = 0; i < 2; ++i)
         if (o->reserved[i]) return fail(MOE_ERR_INVALID, "reserved options must be zero");
     return MOE_OK;
@@ -218,24 +241,35 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
                ev_start = st->sync_ev[3];
     hipEvent_t *ev_g = &st->sync_ev[4], *ev_m = ev_g + PN;
 
-    const bool timing = (o->flags & MOE_FLAG_TIMING) != 0;
+    const bool timing = (o->flags & (MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM)) != 0;
     if (timing) g_timing = TimingRecord{};
-    Timer tm(st, timing);
+    Timer tm(st, o->flags);
     hipStream_t s0 = (hipStream_t)stream;
+    // One stage without shared experts has nothing to overlap: every step
+    // runs on the caller's stream (no cross-stream event hops, which cost
+    // tens of microseconds each).  Otherwise gather, GEMMs and combine run
+    // on their own streams so that stages (and the shared FFN) overlap.
+    const bool one_stream = PN == 1 && !has_shared;
+    hipStream_t sg = one_stream ? s0 : st->sg;
+    hipStream_t sm = one_stream ? s0 : st->sm;
+    hipStream_t sc = one_stream ? s0 : st->sc;
     const int H = d.hidden, I = d.inter;
     const int64_t T = d.tokens;
 
     int total_span = -1;
     MOE_TRY(tm.begin(s0, PH_TOTAL, &total_span));
     // shared experts: independent of routing, start at once on the GEMM stream
-    MOE_HIP(hipEventRecord(ev_start, s0));
-    MOE_HIP(hipStreamWaitEvent(st->sm, ev_start, 0));
+    if (!one_stream) {
+        MOE_HIP(hipEventRecord(ev_start, s0));
+        MOE_HIP(hipStreamWaitEvent(sm, ev_start, 0));
+        tm.gap();
+    }
     if (has_shared) {
-        MOE_TRY(tm.begin(st->sm, PH_SHARED));
+        MOE_TRY(tm.begin(sm, PH_SHARED));
         MOE_HIP(launch_dense_gateup(T, H, d.shared_inter, x, shared_gate, shared_up, shared_act,
-                                    st->sm));
-        MOE_HIP(launch_dense_down(T, H, d.shared_inter, shared_act, shared_down, y, st->sm));
-        MOE_TRY(tm.end(st->sm));
+                                    sm));
+        MOE_HIP(launch_dense_down(T, H, d.shared_inter, shared_act, shared_down, y, sm));
+        MOE_TRY(tm.end(sm));
     }
 
     // routing and dispatch indices on the caller stream
@@ -260,6 +294,7 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
                                hipMemcpyDeviceToHost, s0));
         MOE_HIP(hipEventRecord(ev_counts, s0));
         MOE_HIP(hipEventSynchronize(ev_counts));
+        tm.gap();
         hc.assign(st->pinned_counts, st->pinned_counts + NB);
     }
     // the grouped gate/up GEMM can gather its token rows itself while every
@@ -268,10 +303,13 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     int grid = o->gemm_cu_budget > 0 ? o->gemm_cu_budget : device_cu_count();
     grid = std::max(8, (grid / 8) * 8);
 
-    MOE_HIP(hipEventRecord(ev_fork, s0));
-    MOE_HIP(hipStreamWaitEvent(st->sg, ev_fork, 0));
-    MOE_HIP(hipStreamWaitEvent(st->sm, ev_fork, 0));
-    MOE_HIP(hipStreamWaitEvent(st->sc, ev_fork, 0));
+    if (!one_stream) {
+        MOE_HIP(hipEventRecord(ev_fork, s0));
+        MOE_HIP(hipStreamWaitEvent(sg, ev_fork, 0));
+        MOE_HIP(hipStreamWaitEvent(sm, ev_fork, 0));
+        MOE_HIP(hipStreamWaitEvent(sc, ev_fork, 0));
+        tm.gap();
+    }
 
     for (int i = 0; i < PN; ++i) {
         // buckets [b0, b0 + per_stage); their experts start at e_w (weights)
@@ -294,15 +332,18 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
         // rows straight from x through sorted_slot instead
         const bool fold_gather = !dense && fold_ok;
         if (!fold_gather) {
-            MOE_TRY(tm.begin(st->sg, PH_GATHER));
+            MOE_TRY(tm.begin(sg, PH_GATHER));
             MOE_HIP(launch_gather(d, b0, per_stage, off, sorted_slot, x, x_perm, stage_rows,
-                                  st->sg));
-            MOE_TRY(tm.end(st->sg));
+                                  sg));
+            MOE_TRY(tm.end(sg));
         }
-        MOE_HIP(hipEventRecord(ev_g[i], st->sg));
+        if (!one_stream) {
+            MOE_HIP(hipEventRecord(ev_g[i], sg));
+            MOE_HIP(hipStreamWaitEvent(sm, ev_g[i], 0));
+            tm.gap();
+        }
 
         // expert GEMMs
-        MOE_HIP(hipStreamWaitEvent(st->sm, ev_g[i], 0));
         if (dense) {
             if (timing) ++g_timing.dense_stages;
             int64_t r0 = 0;
@@ -311,14 +352,14 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
                 const int64_t rows = hc[b];
                 if (rows > 0) {
                     const int64_t wo = (int64_t)(e_w + b - b0) * I * H;
-                    MOE_TRY(tm.begin(st->sm, PH_GATEUP));
+                    MOE_TRY(tm.begin(sm, PH_GATEUP));
                     MOE_HIP(launch_dense_gateup(rows, H, I, x_perm + r0 * H, w_gate + wo,
-                                                w_up + wo, act + r0 * I, st->sm));
-                    MOE_TRY(tm.end(st->sm));
-                    MOE_TRY(tm.begin(st->sm, PH_DOWN));
+                                                w_up + wo, act + r0 * I, sm));
+                    MOE_TRY(tm.end(sm));
+                    MOE_TRY(tm.begin(sm, PH_DOWN));
                     MOE_HIP(launch_dense_down(rows, H, I, act + r0 * I, w_down + wo,
-                                              y_perm + r0 * H, st->sm));
-                    MOE_TRY(tm.end(st->sm));
+                                              y_perm + r0 * H, sm));
+                    MOE_TRY(tm.end(sm));
                     if (timing) {
                         ++g_timing.gateup_launches;
                         ++g_timing.down_launches;
@@ -332,34 +373,40 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
                 // the grouped kernels index weights from their first expert:
                 // shift the offsets so that expert e_w .. is bucket b0 ..
                 const int32_t *goff = off + (b0 - e_w);
-                MOE_TRY(tm.begin(st->sm, PH_GATEUP));
+                MOE_TRY(tm.begin(sm, PH_GATEUP));
                 MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, fold_gather ? x : x_perm,
                                             fold_gather ? sorted_slot : nullptr, w_gate, w_up,
-                                            act, grid, st->sm));
-                MOE_TRY(tm.end(st->sm));
-                MOE_TRY(tm.begin(st->sm, PH_DOWN));
+                                            act, grid, sm));
+                MOE_TRY(tm.end(sm));
+                MOE_TRY(tm.begin(sm, PH_DOWN));
                 MOE_HIP(launch_group_down(d, e_w, per_stage, goff, act, w_down, y_perm, grid,
-                                          st->sm));
-                MOE_TRY(tm.end(st->sm));
+                                          sm));
+                MOE_TRY(tm.end(sm));
                 if (timing) {
                     ++g_timing.gateup_launches;
                     ++g_timing.down_launches;
                 }
             }
         }
-        MOE_HIP(hipEventRecord(ev_m[i], st->sm));
+        if (!one_stream) {
+            MOE_HIP(hipEventRecord(ev_m[i], sm));
+            MOE_HIP(hipStreamWaitEvent(sc, ev_m[i], 0));
+            tm.gap();
+        }
 
         // weighted combine of this stage: its experts over all tokens, or
         // all experts over its tokens
-        MOE_HIP(hipStreamWaitEvent(st->sc, ev_m[i], 0));
-        MOE_TRY(tm.begin(st->sc, PH_COMBINE));
+        MOE_TRY(tm.begin(sc, PH_COMBINE));
         const int accumulate = (has_shared || (!tok_stages && i > 0)) ? 1 : 0;
         MOE_HIP(launch_combine(d, tok_stages ? 0 : b0, tok_stages ? EL : per_stage, t_lo, t_hi,
-                               y_perm, ids, slot_row, wts, y, accumulate, st->sc));
-        MOE_TRY(tm.end(st->sc));
+                               y_perm, ids, slot_row, wts, y, accumulate, sc));
+        MOE_TRY(tm.end(sc));
     }
-    MOE_HIP(hipEventRecord(ev_done, st->sc));
-    MOE_HIP(hipStreamWaitEvent(s0, ev_done, 0));
+    if (!one_stream) {
+        MOE_HIP(hipEventRecord(ev_done, sc));
+        MOE_HIP(hipStreamWaitEvent(s0, ev_done, 0));
+        tm.gap();
+    }
     MOE_TRY(tm.end(s0, total_span));
     if (timing) g_timing.valid = true;
     return MOE_OK;

@@ -203,6 +203,29 @@ def test_forward_invariant_to_pipeline_and_gemm_kind(name):
     assert torch.equal(y, base), "CU budget changes the bits"
 
 
+@pytest.mark.parametrize("name", ["ragged8", "fine"])
+def test_forward_timing_modes(name):
+    """Timing every phase or only the GEMMs leaves the result unchanged; the
+    GEMM-only mode reports GEMM time and zero for the other phases, on one
+    stream (PN = 1) and across streams (PN > 1, shared experts)."""
+    inp, _, _ = case(name)
+    g = Dev(inp)
+    base = g.forward(moe.opts()).y.clone()
+    for pn in (1, 2):
+        y = g.forward(moe.opts(pipeline_n=pn, timing=True)).y
+        t_all = moe.last_timing()
+        assert torch.equal(y, base)
+        y = g.forward(moe.opts(pipeline_n=pn, timing="gemm")).y
+        t_gemm = moe.last_timing()
+        assert torch.equal(y, base)
+        assert t_all["route_ms"] > 0 and t_all["combine_ms"] > 0 and t_all["total_ms"] > 0
+        assert t_gemm["route_ms"] == 0 and t_gemm["combine_ms"] == 0 and t_gemm["total_ms"] == 0
+        assert t_gemm["gateup_ms"] > 0 and t_gemm["down_ms"] > 0
+        assert t_gemm["gateup_launches"] == t_all["gateup_launches"] >= 1
+        if inp.shape.n_shared:
+            assert t_gemm["shared_ms"] > 0
+
+
 @pytest.mark.parametrize("name", ["ragged8", "fine", "one"])
 def test_forward_token_range_stages(name):
     """Token-range stages (each stage all experts over a token range, weights

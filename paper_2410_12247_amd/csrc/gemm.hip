@@ -325,6 +325,8 @@ __device__ __forceinline__ void run_tile(const TileArgs &a, bf16_t *smem) {
 // 36 KiB stages) is the largest that fits 256 registers and 160 KiB of LDS.
 // ---------------------------------------------------------------------------
 constexpr int PP_THREADS = 512;
+// buffer resource word 3 for raw (untyped, unswizzled) access on gfx9 parts
+constexpr int kBufferFlags = 0x00020000;
 
 template <int MODE, int BM_>
 struct PPCfg {
@@ -405,21 +407,24 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
     const int x_lds = C::STAGE_W + x_row0 * BK;
     // this wave's share of stage kstage (clamped); nx: its token-row
     // instruction count (the group's)
+    // buffer resources over the weight rows and the token rows: a 32-bit
+    // per-lane row offset plus the stage's k offset as the scalar offset
+    const __amdgpu_buffer_rsrc_t wres =
+        __builtin_amdgcn_make_buffer_rsrc((void *)wsrc, 0, -1, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t xres =
+        __builtin_amdgcn_make_buffer_rsrc((void *)a.x, 0, -1, kBufferFlags);
     auto issue = [&](int kstage, auto nx) {
         const int ks = min(kstage, nk - 1);
         bf16_t *sb = smem + (kstage % NS) * C::STAGE;
-        const char *wk = reinterpret_cast<const char *>(wsrc + ks * BK);
-        const char *xk = reinterpret_cast<const char *>(a.x + ks * BK);
+        const int kb = ks * BK * 2;
 #pragma unroll
         for (int i = 0; i < C::W_INSTR; ++i)
-            __builtin_amdgcn_global_load_lds((gbl_void_t *)(wk + woff[i]),
-                                             (lds_void_t *)(sb + w_lds + i * C::RPI * BK), 16,
-                                             0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                wres, (lds_void_t *)(sb + w_lds + i * C::RPI * BK), 16, woff[i], kb, 0, 0);
 #pragma unroll
         for (int i = 0; i < decltype(nx)::value; ++i)
-            __builtin_amdgcn_global_load_lds((gbl_void_t *)(xk + xoff[i]),
-                                             (lds_void_t *)(sb + x_lds + i * C::RPI * BK), 16,
-                                             0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                xres, (lds_void_t *)(sb + x_lds + i * C::RPI * BK), 16, xoff[i], kb, 0, 0);
     };
 
     // ---- fragments of this wave
@@ -619,9 +624,12 @@ __global__ __launch_bounds__(TP::THREADS) void group_kernel(
     const int32_t *__restrict__ row_map, int slot_div, const bf16_t *w0s, const bf16_t *w1s,
     int64_t wstride, int N, int K, void *out, int64_t ldo) {
     constexpr int BM = TP::BM;
-    __shared__ __attribute__((aligned(16))) bf16_t smem[TP::LDS_ELEMS];
-    __shared__ int s_off[kMaxExperts + 1];
-    __shared__ int s_pre[kMaxExperts + 1];
+    // one LDS object (stage buffers, then the per-expert offsets and tile
+    // prefix sums): the compiler then does not make fragment reads wait for
+    // the LDS-DMA in flight
+    __shared__ __attribute__((aligned(16))) bf16_t smem[TP::LDS_ELEMS + 4 * (kMaxExperts + 1)];
+    int *s_off = reinterpret_cast<int *>(smem + TP::LDS_ELEMS);
+    int *s_pre = s_off + (kMaxExperts + 1);
     const int tid = threadIdx.x;
     const int NT = (N + TP::BNOUT - 1) / TP::BNOUT;
 

@@ -11,12 +11,15 @@
 // 8-byte bf16 store (gate/up), and for gate/up the matching gate and up
 // values sit in the same lane, so SiLU*mul needs no data movement.
 //
-// Workgroup tile: BN weight rows x BM token rows, 4 waves (2 x 2), each wave
-// (BN/2) x (BM/2) built from v_mfma_f32_16x16x32_bf16 with its accumulators
-// in AGPRs.  K advances BK per stage through NS LDS stages filled by
-// LDS-DMA loads, so the loads of the next NS-1 stages are in flight while a
-// stage is multiplied.  16-byte chunks of each LDS row are XOR-swizzled so
-// MFMA operand reads hit distinct banks.
+// Workgroup tile (the one both schedulers use): 256 weight rows x 320 token
+// rows, eight waves in two groups that alternate between MFMAs and memory
+// work (the "ping-pong" tile below), built from v_mfma_f32_16x16x32_bf16.
+// K advances 32 per stage through four LDS stages filled by LDS-DMA loads,
+// so the loads of the next three stages are in flight while a stage is
+// multiplied.  16-byte chunks of each LDS row are XOR-swizzled so MFMA
+// operand reads hit distinct banks.  A four-wave tile (2 x 2 waves, one per
+// SIMD, accumulators in AGPRs) is kept as the alternative selected with
+// MOE_GEMM_PINGPONG=0; it is slower on the expert shapes measured.
 //
 // Two schedulers share that tile code and its arithmetic (so both give the
 // same bits for the same rows):

@@ -25,8 +25,13 @@
  *   hidden, inter and shared_inter multiples of 64, local experts
  *   [local_begin, local_begin + local_count) inside [0, experts),
  *   tokens * top_k < 2^31.
- * - Results are deterministic: the same inputs give the same bits on every
- *   run, for any pipeline number and either GEMM kind.
+ * - Results are deterministic: the same inputs and options give the same
+ *   bits on every run.  With MOE_FLAG_EXACT_ORDER (and in moe_ffn_group and
+ *   moe_ffn_dense) every expert-GEMM output is one pass over K, so the bits
+ *   are also the same for any pipeline number, stage kind, CU budget and
+ *   either GEMM kind.  Without it the grouped GEMM may cut the tiles of its
+ *   last, partial round into K pieces summed in a fixed order, which moves
+ *   the last bits of those outputs with the launch's tile count.
  */
 #ifndef MOE_H
 #define MOE_H
@@ -66,7 +71,7 @@ typedef struct {
 
 enum { MOE_GEMM_AUTO = 0, MOE_GEMM_GROUP = 1, MOE_GEMM_DENSE = 2 };
 enum { MOE_CHUNK_EXPERTS = 0, MOE_CHUNK_TOKENS = 1 };
-enum { MOE_FLAG_TIMING = 1, MOE_FLAG_TIMING_GEMM = 2 };
+enum { MOE_FLAG_TIMING = 1, MOE_FLAG_TIMING_GEMM = 2, MOE_FLAG_EXACT_ORDER = 4 };
 
 /* Options of moe_ffn_forward (Sec. 4.3 of the paper: the GroupGemm /
  * DenseGemm switch by load, the pipeline number PN and how the work is cut
@@ -79,7 +84,7 @@ enum { MOE_FLAG_TIMING = 1, MOE_FLAG_TIMING_GEMM = 2 };
  *   [s*ceil(T/PN), (s+1)*ceil(T/PN)) over all local experts, so every stage
  *   reads every local expert's weights again (the split the paper argues
  *   against); kept as a measured comparison.  Needs PN*local_count <= 256.
- * Both modes give the same bits. */
+ * Both modes give the same bits under MOE_FLAG_EXACT_ORDER. */
 typedef struct {
     int32_t gemm_mode;      /* MOE_GEMM_AUTO, _GROUP or _DENSE */
     int32_t dense_min_rows; /* AUTO picks DenseGemm for a pipeline stage when
@@ -97,7 +102,11 @@ typedef struct {
                                stream; the other phases read 0.  Every
                                event recorded between two kernels delays
                                the second, so this is the mode to time a
-                               run whose wall time also matters. */
+                               run whose wall time also matters.
+                               MOE_FLAG_EXACT_ORDER: no K split in the
+                               grouped GEMM (see the determinism note at
+                               the top); slower when the tile count leaves
+                               a partial last round of the grid. */
     int32_t chunk_mode;     /* MOE_CHUNK_EXPERTS or MOE_CHUNK_TOKENS */
     int32_t reserved[2];    /* must be zero */
 } moe_opts;
@@ -168,7 +177,9 @@ moe_status moe_gather(const moe_dims *dims, int32_t e_first, int32_t e_count,
  * bf16 MFMA with fp32 accumulation; silu(g) = g / (1 + exp(-g)).
  * w_gate/w_up/w_down point at the stacks of all EL local experts.
  * act [R][I] bf16 (caller scratch, rows indexed like x_perm);
- * y_perm [R][H] fp32.  cu_budget: persistent grid size (0 = all CUs). */
+ * y_perm [R][H] fp32.  cu_budget: persistent grid size (0 = all CUs).
+ * Takes no workspace, so every tile is one pass over K (the bits of
+ * moe_ffn_forward with MOE_FLAG_EXACT_ORDER). */
 moe_status moe_ffn_group(const moe_dims *dims, int32_t e_first, int32_t e_count,
                          const int32_t *offsets, const moe_bf16 *x_perm,
                          const moe_bf16 *w_gate, const moe_bf16 *w_up,

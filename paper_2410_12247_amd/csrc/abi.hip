@@ -89,6 +89,8 @@ WsLayout ws_layout(const moe_dims *d, bool forward, int nbuckets) {
         L.act = take(sizeof(bf16_t) * L.rcap * d->inter);
         L.y_perm = take(sizeof(float) * L.rcap * d->hidden);
         L.shared_act = take(sizeof(bf16_t) * T * d->shared_inter);
+        L.split_part = take(gemm_split_bytes());
+        L.split_meta = take(sizeof(int32_t) * kSplitMetaInts);
     }
     L.total = o;
     return L;
@@ -199,9 +201,11 @@ moe_status moe_ffn_group(const moe_dims *dims, int32_t e_first, int32_t e_count,
     int grid = cu_budget > 0 ? cu_budget : device_cu_count();
     grid = std::max(8, (grid / 8) * 8);
     hipStream_t s = (hipStream_t)stream;
-    MOE_HIP(launch_group_gateup(*dims, e_first, e_count, offsets, x_perm, nullptr, w_gate, w_up, act,
-                                grid, s));
-    MOE_HIP(launch_group_down(*dims, e_first, e_count, offsets, act, w_down, y_perm, grid, s));
+    // no workspace here: every tile covers the whole K range in one pass
+    MOE_HIP(launch_group_gateup(*dims, e_first, e_count, offsets, x_perm, nullptr, w_gate, w_up,
+                                act, grid, nullptr, nullptr, s));
+    MOE_HIP(launch_group_down(*dims, e_first, e_count, offsets, act, w_down, y_perm, grid,
+                              nullptr, nullptr, s));
     return MOE_OK;
 }
 

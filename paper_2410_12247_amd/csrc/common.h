@@ -14,6 +14,7 @@ using bf16_t = uint16_t;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMaxExperts = 256;
 constexpr int kMaxTopK = 8;
@@ -60,6 +61,8 @@ struct WsLayout {
     size_t act;           // bf16  [Rcap][I]
     size_t y_perm;        // fp32  [Rcap][H]
     size_t shared_act;    // bf16  [T][Is]
+    size_t split_part;    // fp32  grouped-GEMM K-split partials (gemm_split_bytes)
+    size_t split_meta;    // int32 [kSplitMetaInts] K-split tail-tile records
     size_t total;
     int64_t nchunks;
     int64_t rcap;
@@ -72,6 +75,17 @@ int forward_buckets(const moe_dims *d, const moe_opts *o);
 
 // Permutation chunking: slots handled by one workgroup of the histogram pass.
 constexpr int kPermChunk = 1024;
+
+// K split of the grouped GEMM's last, partial round of tiles: at most
+// kSplitMaxPieces pieces per tile, each at least kSplitMinStages K stages
+// long, at most kSplitSlots pieces (partial-accumulator buffers) in all, so
+// at most kSplitSlots / 2 tiles cut.
+constexpr int kSplitMaxPieces = 8;
+constexpr int kSplitMinStages = 32;
+constexpr int kSplitSlots = 256;
+constexpr int kSplitMetaInts = 2 + 4 * (kSplitSlots / 2);
+// Bytes of the partial-accumulator buffer the grouped GEMM takes (all slots).
+size_t gemm_split_bytes();
 
 // ---- kernel launchers (stream-ordered, no host synchronisation) ----------
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
@@ -97,13 +111,20 @@ hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, int64_t t
 // (row_map NULL: x_rows is x_perm) or straight from the token matrix
 // (x_rows = x, row r is token row_map[r] / top_k, row_map = sorted_slot);
 // the latter needs T*H*2 < 2^32 (byte offsets are 32-bit).
+// parts / split_meta: gemm_split_bytes() and kSplitMetaInts int32 of
+// scratch, or NULL: with them the tiles of the last, partial round of the
+// persistent grid may be cut along K (then a fixup kernel follows the GEMM
+// on the same stream); without them every tile is one pass over K.
+// Launches that share the scratch must not overlap.
 hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
                                const int32_t *offsets, const bf16_t *x_rows,
                                const int32_t *row_map, const bf16_t *w_gate,
-                               const bf16_t *w_up, bf16_t *act, int grid, hipStream_t s);
+                               const bf16_t *w_up, bf16_t *act, int grid, float *parts,
+                               int32_t *split_meta, hipStream_t s);
 hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
                              const int32_t *offsets, const bf16_t *act,
-                             const bf16_t *w_down, float *y_perm, int grid, hipStream_t s);
+                             const bf16_t *w_down, float *y_perm, int grid, float *parts,
+                             int32_t *split_meta, hipStream_t s);
 // Dense GEMMs over `rows` host-known contiguous rows.
 hipError_t launch_dense_gateup(int64_t rows, int H, int I, const bf16_t *x, const bf16_t *w_gate,
                                const bf16_t *w_up, bf16_t *act, hipStream_t s);

@@ -162,7 +162,7 @@ moe_status check_opts(const moe_dims *d, const moe_opts *o) {
         return fail(MOE_ERR_UNSUPPORTED, "token stages: pipeline_n * local_count > %d",
                     kMaxExperts);
     if (o->gemm_cu_budget < 0) return fail(MOE_ERR_INVALID, "gemm_cu_budget < 0");
-    if (o->flags & ~(MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM))
+    if (o->flags & ~(MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM | MOE_FLAG_EXACT_ORDER))
         return fail(MOE_ERR_INVALID, "unknown flags 0x%x", o->flags);
     for (int i = 0; i < 2; ++i)
         if (o->reserved[i]) return fail(MOE_ERR_INVALID, "reserved options must be zero");
@@ -278,6 +278,11 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     MOE_TRY(tm.end(s0));
     MOE_TRY(tm.begin(s0, PH_PERMUTE));
     MOE_HIP(launch_permute(d, ids, ws, L, tps, cnt, off, cnt_el, sorted_slot, slot_row, s0));
+    // K-split scratch of the grouped GEMMs (all on the GEMM stream, one
+    // after another)
+    const bool split = (o->flags & MOE_FLAG_EXACT_ORDER) == 0;
+    float *split_part = split ? reinterpret_cast<float *>(base + L.split_part) : nullptr;
+    int32_t *split_meta = split ? reinterpret_cast<int32_t *>(base + L.split_meta) : nullptr;
     MOE_TRY(tm.end(s0));
 
     // GEMM kind per stage needs the row counts on the host
@@ -376,11 +381,11 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
                 MOE_TRY(tm.begin(sm, PH_GATEUP));
                 MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, fold_gather ? x : x_perm,
                                             fold_gather ? sorted_slot : nullptr, w_gate, w_up,
-                                            act, grid, sm));
+                                            act, grid, split_part, split_meta, sm));
                 MOE_TRY(tm.end(sm));
                 MOE_TRY(tm.begin(sm, PH_DOWN));
                 MOE_HIP(launch_group_down(d, e_w, per_stage, goff, act, w_down, y_perm, grid,
-                                          sm));
+                                          split_part, split_meta, sm));
                 MOE_TRY(tm.end(sm));
                 if (timing) {
                     ++g_timing.gateup_launches;

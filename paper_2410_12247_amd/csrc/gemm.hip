@@ -31,6 +31,7 @@
 // Both map workgroups to tiles XCD by XCD (the hardware deals workgroups
 // round-robin over the 8 XCDs), so the tiles running on one XCD are
 // neighbours in (m, n) and share activation and weight rows in its L2.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -90,9 +91,14 @@ struct TileArgs {
                           // folded into the operand loads)
     int slot_div;
     int m_valid;       // token rows valid from x
-    int K;
+    int K;             // row length of both operands (elements)
+    int k0, nks;       // K stages [k0, k0 + nks) of BK elements this call covers
     void *out;         // output element (first token row, first column)
     int64_t ldo;       // output row stride in elements
+    // K split (npieces > 1): this call is piece `piece` of the tile and
+    // stores its fp32 accumulators in part[piece] instead of the output
+    float *part;
+    int piece, npieces;
 };
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
@@ -351,7 +357,58 @@ struct PPCfg {
     static constexpr int STAGE_W = BN * BK, STAGE_X = BM * BK, STAGE = STAGE_W + STAGE_X;
     static constexpr int LDS_ELEMS = NS * STAGE;
     static constexpr int BNOUT = MODE == 0 ? BN / 2 : BN;
+    static constexpr int PART_ELEMS = BN * BM;  // fp32 accumulators of one tile
+    static constexpr int PART_BYTES = PART_ELEMS * 4;
+    static constexpr int WAVE_BYTES = TN * TM * 1024;  // one wave's block of them
 };
+
+// Epilogue of a ping-pong tile (or of the sum of its K pieces), one 16x16
+// output fragment at a time; the lane holds output columns col..col+3 of
+// token row `row`.  gate/up: fragment (p, m) of wave (wn, wm) from the
+// matching gate and up accumulators, stored as bf16(silu(g) * u).
+template <class C>
+__device__ __forceinline__ void store_gateup(const floatx4 &g, const floatx4 &u, int p, int m,
+                                             int wn, int wm, int lane, bf16_t *out, int64_t ldo,
+                                             int m_valid, int n_valid) {
+    const int row = wm * C::WTM + m * 16 + (lane & 15);
+    const int col = wn * (C::WTN / 2) + p * 16 + (lane >> 4) * 4;
+    if (row < m_valid && col < n_valid) {
+        uint2 v;
+        v.x = pack_bf16x2(silu_mul(g[0], u[0]), silu_mul(g[1], u[1]));
+        v.y = pack_bf16x2(silu_mul(g[2], u[2]), silu_mul(g[3], u[3]));
+        *reinterpret_cast<uint2 *>(out + row * ldo + col) = v;
+    }
+}
+// down: fragment (t, m) of wave (wn, wm), the fp32 values.
+template <class C>
+__device__ __forceinline__ void store_down(const floatx4 &v, int t, int m, int wn, int wm,
+                                           int lane, float *out, int64_t ldo, int m_valid,
+                                           int n_valid) {
+    const int row = wm * C::WTM + m * 16 + (lane & 15);
+    const int col = wn * C::WTN + t * 16 + (lane >> 4) * 4;
+    if (row < m_valid && col < n_valid) *reinterpret_cast<floatx4 *>(out + row * ldo + col) = v;
+}
+
+template <int MODE, class C>
+__device__ __forceinline__ void pp_epilogue(const floatx4 (&acc)[C::TN][C::TM], int wn, int wm,
+                                            int lane, void *outp, int64_t ldo, int m_valid,
+                                            int n_valid) {
+    if (MODE == 0) {
+#pragma unroll
+        for (int p = 0; p < C::TN / 2; ++p)
+#pragma unroll
+            for (int m = 0; m < C::TM; ++m)
+                store_gateup<C>(acc[p][m], acc[p + C::TN / 2][m], p, m, wn, wm, lane,
+                                reinterpret_cast<bf16_t *>(outp), ldo, m_valid, n_valid);
+    } else {
+#pragma unroll
+        for (int t = 0; t < C::TN; ++t)
+#pragma unroll
+            for (int m = 0; m < C::TM; ++m)
+                store_down<C>(acc[t][m], t, m, wn, wm, lane, reinterpret_cast<float *>(outp), ldo,
+                              m_valid, n_valid);
+    }
+}
 
 template <int MODE, int BM_>
 __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
@@ -364,7 +421,7 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
     const int wn = wave & 1;    // weight half
     const int wm = wave >> 1;   // 64-row token block
     const int K = a.K;
-    const int nk = K / BK;
+    const int nk = a.nks;
     // a wave whose token rows or weight rows all lie past the valid edge of
     // a partial tile skips its MFMAs (its outputs are never stored); it still
     // takes its share of the loads and barriers
@@ -419,7 +476,7 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
     auto issue = [&](int kstage, auto nx) {
         const int ks = min(kstage, nk - 1);
         bf16_t *sb = smem + (kstage % NS) * C::STAGE;
-        const int kb = ks * BK * 2;
+        const int kb = (a.k0 + ks) * BK * 2;
 #pragma unroll
         for (int i = 0; i < C::W_INSTR; ++i)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -519,39 +576,25 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
     wait_vmcnt<0>();  // clamped tail requests drained before LDS is reused
     __builtin_amdgcn_s_barrier();
 
-    // ---- epilogue: lane holds output columns col..col+3 of token row `row`
-    const int lcol4 = (lane >> 4) * 4;
-    if (MODE == 0) {
-        bf16_t *out = reinterpret_cast<bf16_t *>(a.out);
+    // ---- K split: the piece stores its accumulators (each wave its own
+    // block, one 1 KiB store per fragment, through a buffer resource so the
+    // fragment offsets are scalars); split_fixup_kernel adds the pieces and
+    // runs the epilogue
+    if (a.npieces > 1) {
+        const __amdgpu_buffer_rsrc_t pres =
+            __builtin_amdgcn_make_buffer_rsrc(a.part, 0, -1, kBufferFlags);
+        const int loff = lane * 16;
 #pragma unroll
-        for (int t = 0; t < C::TN / 2; ++t) {
-            const int col = wn * (C::WTN / 2) + t * 16 + lcol4;
+        for (int t = 0; t < C::TN; ++t)
 #pragma unroll
-            for (int m = 0; m < C::TM; ++m) {
-                const int row = wm * C::WTM + m * 16 + lrow;
-                if (row < a.m_valid && col < a.n_valid) {
-                    const floatx4 g = acc[t][m];
-                    const floatx4 u = acc[t + C::TN / 2][m];
-                    uint2 v;
-                    v.x = pack_bf16x2(silu_mul(g[0], u[0]), silu_mul(g[1], u[1]));
-                    v.y = pack_bf16x2(silu_mul(g[2], u[2]), silu_mul(g[3], u[3]));
-                    *reinterpret_cast<uint2 *>(out + row * a.ldo + col) = v;
-                }
-            }
-        }
-    } else {
-        float *out = reinterpret_cast<float *>(a.out);
-#pragma unroll
-        for (int t = 0; t < C::TN; ++t) {
-            const int col = wn * C::WTN + t * 16 + lcol4;
-#pragma unroll
-            for (int m = 0; m < C::TM; ++m) {
-                const int row = wm * C::WTM + m * 16 + lrow;
-                if (row < a.m_valid && col < a.n_valid)
-                    *reinterpret_cast<floatx4 *>(out + row * a.ldo + col) = acc[t][m];
-            }
-        }
+            for (int m = 0; m < C::TM; ++m)
+                __builtin_amdgcn_raw_buffer_store_b128(
+                    __builtin_bit_cast(u32x4, acc[t][m]), pres, loff,
+                    a.piece * C::PART_BYTES + wave * C::WAVE_BYTES + (t * C::TM + m) * 1024, 0);
+        return;
     }
+
+    pp_epilogue<MODE, C>(acc, wn, wm, lane, a.out, a.ldo, a.m_valid, a.n_valid);
 }
 
 // Tile order inside one expert: super-columns of GROUP_N n-tiles, walked
@@ -573,17 +616,23 @@ struct FourWave {
     static constexpr int BM = BM_;
     static constexpr int BNOUT = C::BNOUT;
     static constexpr int LDS_ELEMS = NS * C::STAGE;
+    static constexpr int KSTEP = BK;
+    static constexpr bool CAN_SPLIT = false;  // covers the whole K range only
+    static constexpr int PART_ELEMS = 0;
     static __device__ __forceinline__ void run(const TileArgs &a, bf16_t *smem) {
         run_tile<MODE, BN_, BM_, BK, NS>(a, smem);
     }
 };
 template <int MODE, int BM_>
 struct PingPong {
-    using C = PPCfg<MODE, BM_>;
+    using C = PPCfg<MODE, BM_>;  // also read by split_fixup_kernel
     static constexpr int THREADS = PP_THREADS;
     static constexpr int BM = C::BM;
     static constexpr int BNOUT = C::BNOUT;
     static constexpr int LDS_ELEMS = C::LDS_ELEMS;
+    static constexpr int KSTEP = C::BK;
+    static constexpr bool CAN_SPLIT = true;
+    static constexpr int PART_ELEMS = C::PART_ELEMS;
     static __device__ __forceinline__ void run(const TileArgs &a, bf16_t *smem) {
         run_tile_pp<MODE, BM_>(a, smem);
     }
@@ -613,7 +662,12 @@ __global__ __launch_bounds__(TP::THREADS) void dense_kernel(const bf16_t *__rest
     a.slot_div = 1;
     a.m_valid = (int)min<int64_t>(BM, rows - m0);
     a.K = K;
+    a.k0 = 0;
+    a.nks = K / TP::KSTEP;
     a.ldo = ldo;
+    a.part = nullptr;
+    a.piece = 0;
+    a.npieces = 1;
     if (MODE == 0)
         a.out = reinterpret_cast<bf16_t *>(out) + m0 * ldo + n0;
     else
@@ -625,7 +679,8 @@ template <int MODE, class TP>
 __global__ __launch_bounds__(TP::THREADS) void group_kernel(
     const int32_t *__restrict__ offsets, int e_first, int e_count, const bf16_t *__restrict__ x,
     const int32_t *__restrict__ row_map, int slot_div, const bf16_t *w0s, const bf16_t *w1s,
-    int64_t wstride, int N, int K, void *out, int64_t ldo) {
+    int64_t wstride, int N, int K, void *out, int64_t ldo, float *__restrict__ parts,
+    int32_t *__restrict__ split_meta) {
     constexpr int BM = TP::BM;
     // one LDS object (stage buffers, then the per-expert offsets and tile
     // prefix sums): the compiler then does not make fragment reads wait for
@@ -655,7 +710,32 @@ __global__ __launch_bounds__(TP::THREADS) void group_kernel(
 
     const int G = gridDim.x;  // multiple of NXCD
     const int slot = (blockIdx.x % NXCD) * (G / NXCD) + blockIdx.x / NXCD;
-    for (int tau = slot; tau < total; tau += G) {
+    const int nk = K / TP::KSTEP;
+    // Tiles [0, full) fill whole rounds of the grid.  The rem < G tiles left
+    // would occupy rem workgroups for one more tile time while the others
+    // idle; with a split buffer they are cut along K into S pieces each
+    // (slots [S*j, S*j + S) take tail tile j = tau - full), so the last round
+    // is about S times shorter.  The pieces store fp32 partial sums;
+    // split_fixup_kernel, launched next, adds them in piece order and
+    // writes the outputs.  split_meta: [0] tail tiles cut (0: none), [1] S,
+    // then per tail tile its first output row, first output column and
+    // valid rows and columns.
+    const int full = total - total % G;
+    const int rem = total - full;
+    int S = 1;
+    if (TP::CAN_SPLIT && parts != nullptr && rem > 0)
+        S = min(min(kSplitMaxPieces, G / rem), min(nk / kSplitMinStages, kSplitSlots / rem));
+    if (S < 2) S = 1;
+    if (split_meta != nullptr && slot == 0 && tid == 0) {
+        split_meta[0] = S > 1 ? rem : 0;
+        split_meta[1] = S;
+    }
+    const int end = S > 1 ? full : total;
+    const int units = S > 1 ? full + rem * S : total;
+    for (int u = slot; u < units; u += G) {
+        const int tau = u < end ? u : full + (u - full) / S;
+        const int piece = u < end ? 0 : (u - full) % S;
+        const int pieces = u < end ? 1 : S;
         // expert: last e with s_pre[e] <= tau
         int lo = 0, hi = e_count - 1;
         while (lo < hi) {
@@ -679,12 +759,110 @@ __global__ __launch_bounds__(TP::THREADS) void group_kernel(
         a.slot_div = slot_div;
         a.m_valid = min(BM, cnt - mt * BM);
         a.K = K;
+        // piece p of S covers stages [p*nk/S, (p+1)*nk/S)
+        a.k0 = piece * nk / pieces;
+        a.nks = (piece + 1) * nk / pieces - a.k0;
         a.ldo = ldo;
         if (MODE == 0)
             a.out = reinterpret_cast<bf16_t *>(out) + r0 * ldo + n0;
         else
             a.out = reinterpret_cast<float *>(out) + r0 * ldo + n0;
+        const int j = tau - full;  // tail tile index when split
+        a.part = pieces > 1 ? parts + (size_t)j * S * TP::PART_ELEMS : nullptr;
+        a.piece = piece;
+        a.npieces = pieces;
+        if (pieces > 1 && piece == 0 && tid == 0) {
+            int32_t *md = split_meta + 2 + 4 * j;
+            md[0] = (int32_t)r0;
+            md[1] = (int32_t)n0;
+            md[2] = a.m_valid;
+            md[3] = a.n_valid;
+        }
         TP::run(a, smem);
+    }
+}
+
+// The fragment rows of one (GEMM wave, fragment-row pair) of a tail tile
+// cut into S pieces: each fragment's S pieces are loaded together and added
+// in piece order, one fragment row at a time.
+template <int MODE, class C, int S>
+__device__ __forceinline__ void fixup_rows(__amdgpu_buffer_rsrc_t pres, int loff, int wave, int p,
+                                           void *o, int64_t ldo, int m_valid, int n_valid) {
+    static_assert(S >= 2 && S <= kSplitMaxPieces, "piece count");
+    constexpr int NP = C::TN / 2;
+#pragma unroll 1
+    for (int m = 0; m < C::TM; ++m) {
+        floatx4 sum[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int f = wave * C::WAVE_BYTES + ((p + h * NP) * C::TM + m) * 1024;
+            floatx4 v[S];
+#pragma unroll
+            for (int q = 0; q < S; ++q)
+                v[q] = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                       pres, loff, q * C::PART_BYTES + f, 0));
+            floatx4 r = v[0];
+#pragma unroll
+            for (int q = 1; q < S; ++q) {
+                r[0] += v[q][0];
+                r[1] += v[q][1];
+                r[2] += v[q][2];
+                r[3] += v[q][3];
+            }
+            sum[h] = r;
+        }
+        const int lane = threadIdx.x & 63;
+        if (MODE == 0) {
+            store_gateup<C>(sum[0], sum[1], p, m, wave & 1, wave >> 1, lane,
+                            reinterpret_cast<bf16_t *>(o), ldo, m_valid, n_valid);
+        } else {
+            store_down<C>(sum[0], p, m, wave & 1, wave >> 1, lane, reinterpret_cast<float *>(o),
+                          ldo, m_valid, n_valid);
+            store_down<C>(sum[1], p + NP, m, wave & 1, wave >> 1, lane,
+                          reinterpret_cast<float *>(o), ldo, m_valid, n_valid);
+        }
+    }
+}
+
+// Sum of the K pieces of the grouped GEMM's tail tiles, then the tile
+// epilogue.  Work unit = (tail tile, GEMM wave), taken grid-stride by
+// workgroups of four waves, one wave per fragment-row pair of that GEMM
+// wave: it loads a fragment's S pieces together, adds them in piece order
+// (p0 + p1 + ...), so the result is the same whichever piece finished first,
+// and stores the pair as the GEMM's own epilogue would.  With no tail tiles
+// (the host does not know the count) every workgroup returns at once.
+template <int MODE, class TP>
+__global__ __launch_bounds__(256) void split_fixup_kernel(const float *__restrict__ parts,
+                                                         const int32_t *__restrict__ meta,
+                                                         void *out, int64_t ldo) {
+    using C = typename TP::C;
+    constexpr int NP = C::TN / 2;  // fragment-row pairs per wave
+    static_assert(NP * 64 == 256, "one wave per fragment-row pair");
+    const int ntail = meta[0];
+    const int S = meta[1];
+    const int p = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    for (int unit = blockIdx.x; unit < ntail * 8; unit += gridDim.x) {
+        const int j = unit / 8;
+        const int wave = unit % 8;
+        const int32_t *md = meta + 2 + 4 * j;
+        const int64_t r0 = md[0], n0 = md[1];
+        const int m_valid = md[2], n_valid = md[3];
+        const __amdgpu_buffer_rsrc_t pres = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(parts) + (size_t)j * S * C::PART_ELEMS, 0, -1, kBufferFlags);
+        const int loff = lane * 16;
+        void *o = MODE == 0 ? (void *)(reinterpret_cast<bf16_t *>(out) + r0 * ldo + n0)
+                            : (void *)(reinterpret_cast<float *>(out) + r0 * ldo + n0);
+        switch (S) {  // a static piece count: loads and sums stay unrolled
+            case 2: fixup_rows<MODE, C, 2>(pres, loff, wave, p, o, ldo, m_valid, n_valid); break;
+            case 3: fixup_rows<MODE, C, 3>(pres, loff, wave, p, o, ldo, m_valid, n_valid); break;
+            case 4: fixup_rows<MODE, C, 4>(pres, loff, wave, p, o, ldo, m_valid, n_valid); break;
+            case 5: fixup_rows<MODE, C, 5>(pres, loff, wave, p, o, ldo, m_valid, n_valid); break;
+            case 6: fixup_rows<MODE, C, 6>(pres, loff, wave, p, o, ldo, m_valid, n_valid); break;
+            case 7: fixup_rows<MODE, C, 7>(pres, loff, wave, p, o, ldo, m_valid, n_valid); break;
+            case 8: fixup_rows<MODE, C, 8>(pres, loff, wave, p, o, ldo, m_valid, n_valid); break;
+            default: break;
+        }
     }
 }
 
@@ -727,26 +905,56 @@ hipError_t launch_dense_down(int64_t rows, int H, int I, const bf16_t *act,
     return hipGetLastError();
 }
 
+size_t gemm_split_bytes() {
+    const size_t e = std::max(GroupTile<0>::PART_ELEMS, GroupTile<1>::PART_ELEMS);
+    return e * sizeof(float) * kSplitSlots;
+}
+
+// Fixup launch after a grouped GEMM that was given a split buffer: at most
+// min(grid, kSplitSlots) / 2 tiles can be cut (each into two or more
+// pieces), 8 work units each; one workgroup per compute unit at most, so an
+// empty fixup is cheap to dispatch.
+template <int MODE, class TP>
+hipError_t launch_split_fixup(int grid, const float *parts, const int32_t *meta, void *out,
+                              int64_t ldo, hipStream_t s) {
+    if constexpr (!TP::CAN_SPLIT) {
+        return hipSuccess;
+    } else {
+        const int max_tail = std::min(grid, kSplitSlots) / 2;
+        const int blocks = std::min(max_tail * 8, device_cu_count());
+        split_fixup_kernel<MODE, TP><<<blocks, 256, 0, s>>>(parts, meta, out, ldo);
+        return hipGetLastError();
+    }
+}
+
 hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
                                const int32_t *offsets, const bf16_t *x_rows,
                                const int32_t *row_map, const bf16_t *w_gate,
-                               const bf16_t *w_up, bf16_t *act, int grid, hipStream_t s) {
+                               const bf16_t *w_up, bf16_t *act, int grid, float *parts,
+                               int32_t *split_meta, hipStream_t s) {
     if (e_count <= 0) return hipSuccess;
     using TP = GroupTile<0>;
+    const bool split = parts != nullptr && split_meta != nullptr;
     group_kernel<0, TP><<<grid, TP::THREADS, 0, s>>>(
         offsets, e_first, e_count, x_rows, row_map, d.top_k, w_gate, w_up,
-        (int64_t)d.inter * d.hidden, d.inter, d.hidden, act, d.inter);
+        (int64_t)d.inter * d.hidden, d.inter, d.hidden, act, d.inter,
+        split ? parts : nullptr, split ? split_meta : nullptr);
+    if (split) return launch_split_fixup<0, TP>(grid, parts, split_meta, act, d.inter, s);
     return hipGetLastError();
 }
 
 hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
                              const int32_t *offsets, const bf16_t *act,
-                             const bf16_t *w_down, float *y_perm, int grid, hipStream_t s) {
+                             const bf16_t *w_down, float *y_perm, int grid, float *parts,
+                             int32_t *split_meta, hipStream_t s) {
     if (e_count <= 0) return hipSuccess;
     using TP = GroupTile<1>;
-    group_kernel<1, TP><<<grid, TP::THREADS, 0, s>>>(offsets, e_first, e_count, act, nullptr, 1,
-                                                     w_down, nullptr, (int64_t)d.hidden * d.inter,
-                                                     d.hidden, d.inter, y_perm, d.hidden);
+    const bool split = parts != nullptr && split_meta != nullptr;
+    group_kernel<1, TP><<<grid, TP::THREADS, 0, s>>>(
+        offsets, e_first, e_count, act, nullptr, 1, w_down, nullptr,
+        (int64_t)d.hidden * d.inter, d.hidden, d.inter, y_perm, d.hidden,
+        split ? parts : nullptr, split ? split_meta : nullptr);
+    if (split) return launch_split_fixup<1, TP>(grid, parts, split_meta, y_perm, d.hidden, s);
     return hipGetLastError();
 }
 

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmoe.so")
 
 GEMM_AUTO, GEMM_GROUP, GEMM_DENSE = 0, 1, 2
 CHUNK_EXPERTS, CHUNK_TOKENS = 0, 1
-FLAG_TIMING, FLAG_TIMING_GEMM = 1, 2
+FLAG_TIMING, FLAG_TIMING_GEMM, FLAG_EXACT_ORDER = 1, 2, 4
 
 # the entry points include/moe.h declares
 EXPORTS = ("moe_workspace_bytes", "moe_route", "moe_permute", "moe_gather", "moe_ffn_group",
@@ -105,12 +105,16 @@ def dims(tokens, hidden, inter, experts, top_k, local_begin=0, local_count=None,
 
 
 def opts(gemm_mode=GEMM_AUTO, dense_min_rows=0, pipeline_n=1, gemm_cu_budget=0,
-         timing=False, chunk_mode=CHUNK_EXPERTS) -> Opts:
-    """timing: False, True (every phase) or "gemm" (the GEMM launches only)."""
+         timing=False, chunk_mode=CHUNK_EXPERTS, exact_order=False) -> Opts:
+    """timing: False, True (every phase) or "gemm" (the GEMM launches only).
+    exact_order: no K split of the grouped GEMM's last round (the same bits
+    for every pipeline number, stage kind, CU budget and GEMM kind)."""
     o = Opts()
     o.gemm_mode, o.dense_min_rows, o.pipeline_n = gemm_mode, dense_min_rows, pipeline_n
     o.gemm_cu_budget = gemm_cu_budget
     o.flags = FLAG_TIMING_GEMM if timing == "gemm" else (FLAG_TIMING if timing else 0)
+    if exact_order:
+        o.flags |= FLAG_EXACT_ORDER
     o.chunk_mode = chunk_mode
     return o
 

@@ -104,11 +104,13 @@ def test_invalid_options_and_buffers_rejected():
                            None, None, None, fake, None, None, None, fake, 1 << 40, None)
     assert st == 1
     o = moe.opts()
-    o.flags = 4  # unknown flag
+    o.flags = 8  # unknown flag
     st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake, fake,
                            None, None, None, fake, None, None, None, fake, 1 << 40, None)
     assert st == 1
     assert moe.opts(timing="gemm").flags == 2 and moe.opts(timing=True).flags == 1
+    assert moe.opts(exact_order=True).flags == 4
+    assert moe.opts(timing="gemm", exact_order=True).flags == 6
     o = moe.opts()
     o.reserved[1] = 5
     st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake, fake,

@@ -37,6 +37,9 @@ WORKLOAD_TEXT = {
             "+ 2 shared experts I=1536",
     "zipf": "DeepSeekV2 local-expert shape, Zipf(1.2) expert popularity: H=5120 E=160 "
             "(20 local) I=1536 top-6",
+    "mixtral_ep": "Mixtral-8x7B EP share (4 GPUs): T=16384 H=4096 E=8 (2 local) I=14336 "
+                  "top-2 renorm",
+    "dbrx_ep": "DBRX EP share (8 GPUs): T=8192 H=6144 E=16 (2 local) I=10752 top-4 renorm",
 }
 
 
@@ -171,6 +174,15 @@ def measured_traffic(workload, kernel_prefix):
     return None
 
 
+def gateup_bytes(s, counts):
+    """Algorithmic HBM bytes of the gate/up GEMMs of one forward: the gate
+    and up weights of every local expert that has rows, read once, the token
+    rows read once per routed row, the activation written once."""
+    active = int((counts > 0).sum())
+    R = int(counts.sum())
+    return 2.0 * active * s.I * s.H * 2 + R * s.H * 2 + R * s.I * 2
+
+
 def phase_bytes(s, R, accumulate):
     """Algorithmic HBM bytes of the memory-bound phases of one forward."""
     return {
@@ -228,8 +240,17 @@ def main(argv=None):
     # events recorded on the GEMM stream around each launch
     per_launch_ms = tm["gateup_ms"] / max(tm["gateup_launches"], 1)
     per_launch_flops = fg / max(tm["gateup_launches"], 1)
-    achieved = per_launch_flops / (per_launch_ms * 1e-3) / 1e12
-    peak = PEAK_BF16_FLOPS / 1e12
+    # bound by MFMA or by HBM: the gate/up GEMM's flops per algorithmic byte
+    # against the machine balance (2.5e15 / 8e12 = 312 flop/B); few tokens
+    # per expert (decode) leave it streaming weights
+    per_launch_bytes = gateup_bytes(shape, counts) / max(tm["gateup_launches"], 1)
+    hbm_bound = fg / max(gateup_bytes(shape, counts), 1.0) < PEAK_BF16_FLOPS / PEAK_HBM_BYTES
+    if hbm_bound:
+        achieved = per_launch_bytes / (per_launch_ms * 1e-3) / 1e9
+        peak = PEAK_HBM_BYTES / 1e9
+    else:
+        achieved = per_launch_flops / (per_launch_ms * 1e-3) / 1e12
+        peak = PEAK_BF16_FLOPS / 1e12
     pb = phase_bytes(shape, R, shape.shared_inter > 0)
     gbps = {k: round(v / (tm[f"{k}_ms"] * 1e-3) / 1e9, 1) for k, v in pb.items()
             if tm[f"{k}_ms"] > 0}
@@ -260,12 +281,14 @@ def main(argv=None):
                    "gemm_mode": args.mode, "pipeline_n": args.pn,
                    "chunk_mode": args.chunk_mode,
                    "gemm_cu_budget": args.cu_budget, "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+        "roofline": {"bound": "hbm" if hbm_bound else "mfma", "achieved": round(achieved, 1),
+                     "peak": peak, "unit": "GB/s" if hbm_bound else "TFLOP/s",
+                     "frac": round(achieved / peak, 4),
                      "traffic": traffic,
                      "kernel": "gate/up GEMM (fused SiLU*mul)",
                      "per_launch_ms": round(per_launch_ms, 4),
-                     "per_launch_gflop": round(per_launch_flops / 1e9, 2)},
+                     "per_launch_gflop": round(per_launch_flops / 1e9, 2),
+                     "per_launch_mb": round(per_launch_bytes / 1e6, 1)},
         "gemm": {"tflops_per_s_wall": round(gemm_flops_total / (ms * 1e-3) / 1e12, 1),
                  "tflops_per_s_busy": round(gemm_flops_total / (gemm_ms * 1e-3) / 1e12, 1),
                  "mfma_frac_busy": round(gemm_flops_total / (gemm_ms * 1e-3) / PEAK_BF16_FLOPS, 4),

@@ -80,6 +80,7 @@ WsLayout ws_layout(const moe_dims *d, bool forward, int nbuckets) {
     if (forward) {
         L.ids = take(sizeof(int32_t) * nslots);
         L.weights = take(sizeof(float) * nslots);
+        L.logits = T <= kRouteStreamMaxTokens ? take(sizeof(float) * T * d->experts) : 0;
         L.counts = take(sizeof(int32_t) * NB);
         L.counts_el = take(sizeof(int32_t) * EL);
         L.offsets = take(sizeof(int32_t) * (NB + 1));
@@ -145,7 +146,8 @@ moe_status moe_route(const moe_dims *dims, const moe_bf16 *x, const float *w_rou
     if (dims->tokens == 0) return MOE_OK;
     if (!x || !w_router || !topk_ids || !topk_w)
         return fail(MOE_ERR_INVALID, "moe_route: NULL tensor");
-    MOE_HIP(launch_route(*dims, x, w_router, bias, topk_ids, topk_w, (hipStream_t)stream));
+    MOE_HIP(launch_route(*dims, x, w_router, bias, topk_ids, topk_w, nullptr,
+                         (hipStream_t)stream));
     return MOE_OK;
 }
 

@@ -52,6 +52,8 @@ struct WsLayout {
     size_t slot_rank;     // int32 [T*k]
     size_t ids;           // int32 [T*k]   (forward, when the caller passes none)
     size_t weights;       // fp32  [T*k]
+    size_t logits;        // fp32  [T][E] router logits when T <= kRouteStreamMaxTokens, else 0
+                          // (chunk_counts is always at offset 0, so 0 means none)
     size_t counts;        // int32 [nbuckets] rows per bucket
     size_t counts_el;     // int32 [EL] rows per local expert (TOKENS stages)
     size_t offsets;       // int32 [nbuckets+1]
@@ -88,8 +90,11 @@ constexpr int kSplitMetaInts = 2 + 4 * (kSplitSlots / 2);
 size_t gemm_split_bytes();
 
 // ---- kernel launchers (stream-ordered, no host synchronisation) ----------
+// logits: [T][E] fp32 scratch (may be NULL) for the many-expert, few-token
+// path (T <= kRouteStreamMaxTokens).
+constexpr int64_t kRouteStreamMaxTokens = 1024;
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
-                        int32_t *ids, float *w, hipStream_t s);
+                        int32_t *ids, float *w, float *logits, hipStream_t s);
 // Dispatch indices.  tokens_per_stage == 0: buckets are the local experts;
 // else bucket = (t / tokens_per_stage) * EL + local expert and counts_el
 // (may be NULL) receives the rows per local expert summed over stages.

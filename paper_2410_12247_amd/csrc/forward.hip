@@ -274,7 +274,8 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
 
     // routing and dispatch indices on the caller stream
     MOE_TRY(tm.begin(s0, PH_ROUTE));
-    MOE_HIP(launch_route(d, x, w_router, bias, ids, wts, s0));
+    float *logits = L.logits ? reinterpret_cast<float *>(base + L.logits) : nullptr;
+    MOE_HIP(launch_route(d, x, w_router, bias, ids, wts, logits, s0));
     MOE_TRY(tm.end(s0));
     MOE_TRY(tm.begin(s0, PH_PERMUTE));
     MOE_HIP(launch_permute(d, ids, ws, L, tps, cnt, off, cnt_el, sorted_slot, slot_row, s0));

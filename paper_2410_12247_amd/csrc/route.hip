@@ -94,6 +94,60 @@ __device__ __forceinline__ float key_logit(uint64_t key) {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
+// Top-k and softmax weights of token t from its E logits (zrow, in LDS),
+// by one wave: lane l holds experts l, l+64, l+128, l+192; each of the k
+// rounds takes the wave-wide max key; the weights are fp64 softmax values
+// rounded once to fp32.
+__device__ __forceinline__ void select_token(const float *zrow, int64_t t, int E, int k,
+                                             int renorm, int lane, int32_t *__restrict__ ids,
+                                             float *__restrict__ wout) {
+    uint64_t key[4];
+    float zl[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int e = lane + 64 * q;
+        zl[q] = e < E ? zrow[e] : 0.0f;
+        key[q] = e < E ? logit_key(zl[q], e) : 0ull;
+    }
+    int sel_e[kMaxTopK];
+    float sel_z[kMaxTopK];
+#pragma unroll
+    for (int j = 0; j < kMaxTopK; ++j) {
+        sel_e[j] = 0;
+        sel_z[j] = 0.0f;
+        if (j < k) {
+            const uint64_t best =
+                wave_max_u64(max_u64(max_u64(key[0], key[1]), max_u64(key[2], key[3])));
+            sel_e[j] = (int)(0xFFFFFFFFu - (uint32_t)best);
+            sel_z[j] = key_logit(best);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (key[q] == best) key[q] = 0ull;
+        }
+    }
+    const double zmax = (double)sel_z[0];
+    double denom;
+    if (renorm) {
+        denom = 0.0;
+#pragma unroll
+        for (int j = 0; j < kMaxTopK; ++j)
+            if (j < k) denom += exp((double)sel_z[j] - zmax);
+    } else {
+        double part = 0.0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (lane + 64 * q < E) part += exp((double)zl[q] - zmax);
+        denom = wave_sum_f64(part);
+    }
+#pragma unroll
+    for (int j = 0; j < kMaxTopK; ++j) {
+        if (j < k && lane == j) {
+            ids[t * k + j] = sel_e[j];
+            wout[t * k + j] = (float)(exp((double)sel_z[j] - zmax) / denom);
+        }
+    }
+}
+
 // Logits phase layout: 256 threads = TG token groups x EG expert groups
 // (EG = 16, or 8 when E <= 8 so that no thread repeats an expert); a thread
 // owns TT tokens (tg + TG i: consecutive lanes read rows 36 floats apart, so
@@ -252,52 +306,131 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
     for (int tt = g * (RT_TOK / 4); tt < (g + 1) * (RT_TOK / 4); ++tt) {
         const int64_t t = t0 + tt;
         if (t >= T) break;
-        uint64_t key[4];
-        float zl[4];
+        select_token(zs + tt * ZLD, t, E, k, renorm, lane, ids, wout);
+    }
+}
+
+// Streaming router: workgroup = TB tokens x EB experts (TB * EB = 256), one
+// fma chain per thread.  x rows (bf16) and router rows (fp32) stream through
+// an LDS ring of RS_NS stages of RS_HS h by LDS-DMA, RS_NS - 1 stages in
+// flight, so the latency of the loads is covered even when each stage holds
+// little work (few tokens, or few experts).  Each wave issues the same
+// number of DMA requests per stage (short waves repeat their last request:
+// the same bytes to the same place), so one vmcnt wait per stage is right
+// for every wave.  x chunks are XOR-swizzled by row so the 16 rows a wave
+// reads at once spread over the banks.
+// The logits go to z [T][E] and route_select_kernel picks.  (A fused form
+// for E <= 16, the workgroup picking the top-k of its tokens itself, was
+// slower than route_kernel at every T.)
+constexpr int RS_HS = 64;  // h per stage
+constexpr int RS_NS = 8;   // stages in the ring
+template <int TB, int EB>
+__global__ __launch_bounds__(RT_THREADS) void route_stream_kernel(
+    const bf16_t *__restrict__ x, const float *__restrict__ wr, const float *__restrict__ bias,
+    int64_t T, int H, int E, float *__restrict__ z) {
+    static_assert(TB * EB == RT_THREADS, "one chain per thread");
+    constexpr int XB = TB * RS_HS * 2;    // bytes of an x stage
+    constexpr int WB = EB * RS_HS * 4;    // bytes of a router stage
+    constexpr int NXI = XB / 1024;        // wave-wide 16-byte DMA requests
+    constexpr int NWI = WB / 1024;
+    constexpr int PER = (NXI + NWI + 3) / 4;  // requests per wave per stage
+    static_assert(XB % 1024 == 0 && WB % 1024 == 0, "stages of whole requests");
+    static_assert((RS_NS - 2) * PER <= 63, "vmcnt range");
+    constexpr int STAGE = XB + WB;
+    __shared__ __attribute__((aligned(16))) char lds[RS_NS * STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int tb = tid % TB;   // token of this thread's chain
+    const int eb = tid / TB;   // expert
+    const int64_t t0 = (int64_t)blockIdx.x * TB;
+    const int e0 = blockIdx.y * EB;
+
+    // this wave's requests: q = wave + 4 j (j < PER), clamped to the last
+    // real one; q < NXI are x requests (8 rows of 128 bytes), the rest
+    // router requests (4 rows of 256 bytes)
+    const char *src[PER];
+    int dst[PER];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int e = lane + 64 * q;
-            zl[q] = e < E ? zs[tt * ZLD + e] : 0.0f;
-            key[q] = e < E ? logit_key(zl[q], e) : 0ull;
-        }
-        int sel_e[kMaxTopK];
-        float sel_z[kMaxTopK];
-#pragma unroll
-        for (int j = 0; j < kMaxTopK; ++j) {
-            sel_e[j] = 0;
-            sel_z[j] = 0.0f;
-            if (j < k) {
-                const uint64_t best =
-                    wave_max_u64(max_u64(max_u64(key[0], key[1]), max_u64(key[2], key[3])));
-                sel_e[j] = (int)(0xFFFFFFFFu - (uint32_t)best);
-                sel_z[j] = key_logit(best);
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    if (key[q] == best) key[q] = 0ull;
-            }
-        }
-        const double zmax = (double)sel_z[0];
-        double denom;
-        if (renorm) {
-            denom = 0.0;
-#pragma unroll
-            for (int j = 0; j < kMaxTopK; ++j)
-                if (j < k) denom += exp((double)sel_z[j] - zmax);
+    for (int j = 0; j < PER; ++j) {
+        const int q = min(wave + 4 * j, NXI + NWI - 1);
+        if (q < NXI) {
+            const int r = q * 8 + (lane >> 3);
+            const int c = (lane & 7) ^ (r & 7);  // 16-byte chunk of the row this lane fetches
+            const int64_t t = min<int64_t>(t0 + r, T - 1);
+            src[j] = reinterpret_cast<const char *>(x + t * H) + c * 16;
+            dst[j] = q * 1024;
         } else {
-            double part = 0.0;
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                if (lane + 64 * q < E) part += exp((double)zl[q] - zmax);
-            denom = wave_sum_f64(part);
-        }
-#pragma unroll
-        for (int j = 0; j < kMaxTopK; ++j) {
-            if (j < k && lane == j) {
-                ids[t * k + j] = sel_e[j];
-                wout[t * k + j] = (float)(exp((double)sel_z[j] - zmax) / denom);
-            }
+            const int qw = q - NXI;
+            const int r = qw * 4 + (lane >> 4);
+            const int e = min(e0 + r, E - 1);  // rows past E: a copy, never used
+            src[j] = reinterpret_cast<const char *>(wr + (int64_t)e * H) + (lane & 15) * 16;
+            dst[j] = XB + qw * 1024;
         }
     }
+    auto issue = [&](int st) {  // stage st into ring slot st % RS_NS
+        const int hb = st * RS_HS;
+        char *slot = lds + (st % RS_NS) * STAGE;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int q = min(wave + 4 * j, NXI + NWI - 1);
+            const int scale = q < NXI ? 2 : 4;  // bytes per element
+            __builtin_amdgcn_global_load_lds((gbl_void_t *)(src[j] + (int64_t)hb * scale),
+                                             (lds_void_t *)(slot + dst[j]), 16, 0, 0);
+        }
+    };
+
+    const int nst = H / RS_HS;
+#pragma unroll
+    for (int st = 0; st < RS_NS - 1; ++st)
+        if (st < nst) issue(st);
+    float acc = 0.0f;
+    for (int st = 0; st < nst; ++st) {
+        // stage st landed (this wave's share; later stages may be in flight)
+        if (st + RS_NS - 2 < nst) {
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"((RS_NS - 2) * PER) : "memory");
+        } else {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+        // every wave's share landed; slot (st - 1) fully read (a plain
+        // barrier: the waits above are the only memory ordering needed, and
+        // a fenced barrier would drain the requests still in flight)
+        __builtin_amdgcn_s_barrier();
+        if (st + RS_NS - 1 < nst) issue(st + RS_NS - 1);
+        const char *slot = lds + (st % RS_NS) * STAGE;
+        const char *xr = slot + tb * (RS_HS * 2);
+        const float *wrow = reinterpret_cast<const float *>(slot + XB) + eb * RS_HS;
+#pragma unroll
+        for (int c = 0; c < RS_HS / 8; ++c) {
+            const uint4 xv = *reinterpret_cast<const uint4 *>(xr + ((c ^ (tb & 7)) * 16));
+            const float4 w0 = *reinterpret_cast<const float4 *>(wrow + c * 8);
+            const float4 w1 = *reinterpret_cast<const float4 *>(wrow + c * 8 + 4);
+            acc = __builtin_fmaf(bf16_lo(xv.x), w0.x, acc);
+            acc = __builtin_fmaf(bf16_hi(xv.x), w0.y, acc);
+            acc = __builtin_fmaf(bf16_lo(xv.y), w0.z, acc);
+            acc = __builtin_fmaf(bf16_hi(xv.y), w0.w, acc);
+            acc = __builtin_fmaf(bf16_lo(xv.z), w1.x, acc);
+            acc = __builtin_fmaf(bf16_hi(xv.z), w1.y, acc);
+            acc = __builtin_fmaf(bf16_lo(xv.w), w1.z, acc);
+            acc = __builtin_fmaf(bf16_hi(xv.w), w1.w, acc);
+        }
+    }
+    const int e = e0 + eb;
+    const int64_t t = t0 + tb;
+    if (e < E && bias) acc = acc + bias[e];
+    if (e < E && t < T) z[t * E + e] = acc;
+}
+
+// Top-k of logits z [T][E] from route_stream_kernel: one wave per token.
+__global__ __launch_bounds__(RT_THREADS) void route_select_kernel(const float *__restrict__ z,
+                                                                  int64_t T, int E, int k,
+                                                                  int renorm,
+                                                                  int32_t *__restrict__ ids,
+                                                                  float *__restrict__ wout) {
+    const int64_t t = (int64_t)blockIdx.x * (RT_THREADS / 64) + (threadIdx.x >> 6);
+    if (t >= T) return;
+    select_token(z + t * E, t, E, k, renorm, threadIdx.x & 63, ids, wout);
 }
 
 template <int TE, int TT, int EG>
@@ -336,10 +469,31 @@ hipError_t launch_te(const moe_dims &d, const bf16_t *x, const float *wr, const 
 
 }  // namespace
 
+template <int EB>
+hipError_t launch_stream(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
+                         int32_t *ids, float *w, float *z, hipStream_t s) {
+    constexpr int TB = RT_THREADS / EB;
+    const dim3 grid((unsigned)((d.tokens + TB - 1) / TB), (unsigned)((d.experts + EB - 1) / EB));
+    route_stream_kernel<TB, EB><<<grid, RT_THREADS, 0, s>>>(x, wr, bias, d.tokens, d.hidden,
+                                                            d.experts, z);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    route_select_kernel<<<(unsigned)((d.tokens + 3) / 4), RT_THREADS, 0, s>>>(
+        z, d.tokens, d.experts, d.top_k, d.renormalize, ids, w);
+    return hipGetLastError();
+}
+
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
-                        int32_t *ids, float *w, hipStream_t s) {
+                        int32_t *ids, float *w, float *logits, hipStream_t s) {
     if (d.tokens <= 0) return hipSuccess;
     if (d.experts <= 8) return launch_te<1, 8>(d, x, wr, bias, ids, w, s);
+    // many experts, few tokens: the register-tiled kernel has too few
+    // workgroups to cover its serial h loop, so the streaming kernel spreads
+    // expert blocks over more workgroups (logits through the caller's
+    // buffer, then the selection kernel).  With E <= 16 the register-tiled
+    // kernel is faster at every T measured (1 to 16384 tokens).
+    if (d.experts > 16 && logits && d.tokens <= kRouteStreamMaxTokens)
+        return launch_stream<16>(d, x, wr, bias, ids, w, logits, s);
     const int te = (d.experts + 15) / 16;
     if (te <= 1) return launch_te<1>(d, x, wr, bias, ids, w, s);
     if (te <= 2) return launch_te<2>(d, x, wr, bias, ids, w, s);

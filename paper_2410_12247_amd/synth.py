@@ -19,6 +19,16 @@ tensors of the same shapes stand in for them):
                 over 160 experts, top-6 softmax over all 160 (no renorm);
                 the 20 local experts [0, 20) of hidden 5120, width 1536 are
                 computed, plus 2 shared experts of width 1536 on every token.
+* ``mixtral_ep`` : Mixtral 8x7B as the paper deploys it with expert
+                parallelism over 4 GPUs: one GPU's 2 local experts [0, 2) of
+                full width 14336 (hidden 4096, top-2 of 8, renorm) over 16384
+                routed tokens (about 8192 rows: the TP shard's GEMM flops).
+* ``dbrx_ep`` : DBRX over 8 GPUs: 2 local experts [0, 2) of width 10752
+                (hidden 6144, top-4 of 16, renorm) over 8192 routed tokens
+                (about 4096 rows: the TP shard's GEMM flops).
+* decode      : any shape at T = 1 .. 64 tokens (``with_tokens``; x is the
+                first draw, so the weights of such a draw differ from the
+                full-T draw's).
 * ``zipf``    : the dsv2 local-expert shape without shared experts, at
                 T in {64, 256, 1024, 4096, 16384, 65536}, with a router bias
                 that gives a Zipf(1.2) popularity over the 160 experts.
@@ -76,6 +86,8 @@ SHAPES = {
                      n_shared=2, Is=1536),
     "zipf": MoEShape("zipf", 4, 16384, 5120, 1536, 160, 20, 6, False,
                      zipf_bias=True),
+    "mixtral_ep": MoEShape("mixtral_ep", 5, 16384, 4096, 14336, 8, 2, 2, True),
+    "dbrx_ep": MoEShape("dbrx_ep", 6, 8192, 6144, 10752, 16, 2, 4, True),
 }
 
 

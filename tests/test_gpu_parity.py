@@ -289,6 +289,29 @@ def test_forward_k_split(name):
         assert_close(yo.cpu().numpy(), ref, f"{name} PN={o.pipeline_n} budget={o.gemm_cu_budget}")
 
 
+@pytest.mark.parametrize("T,E", [(1, 17), (37, 40), (1024, 17), (1024, 160), (1025, 160)])
+def test_forward_routing_many_experts(T, E):
+    """Routing inside the forward for E > 16: up to 1024 tokens the logits come
+    from the streaming router (blocks of 16 experts, a ragged last block when
+    16 does not divide E, the logits through the workspace) and a separate
+    selection; above that from the register-tiled router.  Ids, weights,
+    counts and y match the oracle; duplicated router rows make exact ties,
+    which go to the lower expert index."""
+    shp = C(name=f"many{T}_{E}", index=214, T=T, H=192, I=64, E=E, EL=4, e0=E - 4, k=6,
+            renorm=False)
+    inp = synth.make_inputs(shp)
+    inp.w_router[E - 1] = inp.w_router[3]
+    inp.w_router[9] = inp.w_router[3]
+    inp.w_router[E - 2] = inp.w_router[E - 3]
+    _, ids, w = oracle.route(inp.x, inp.w_router, inp.bias, shp.k, shp.renorm)
+    buf = Dev(inp).forward()
+    assert np.array_equal(buf.topk_ids.cpu().numpy(), ids)
+    assert weights_match(buf.topk_w.cpu().numpy(), w)
+    counts, *_ = oracle.dispatch(ids, shp.e0, shp.EL)
+    assert np.array_equal(buf.counts.cpu().numpy(), counts)
+    assert_close(buf.y.cpu().numpy(), oracle_y(inp, ids, w, np.arange(T)), f"T={T} E={E}")
+
+
 def test_forward_token_stages_hot_expert_and_empty_stages():
     """All rows on one expert, PN larger than the token count leaves empty
     stages; shared experts make every stage accumulate."""

@@ -15,7 +15,9 @@ from gpu_util import Dev, assert_close
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 WORKLOADS = [("tiny", None), ("mixtral", None), ("dbrx", None), ("dsv2", None),
-             ("zipf", 64), ("zipf", 4096), ("zipf", 65536)]
+             ("zipf", 64), ("zipf", 4096), ("zipf", 65536),
+             # expert-parallel shares as the paper deploys them, and decode
+             ("mixtral_ep", None), ("dbrx_ep", None), ("mixtral", 1), ("mixtral", 64)]
 SAMPLE = 24  # tokens per workload checked against the oracle FFN
 
 

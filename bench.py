@@ -65,6 +65,15 @@ def parse_args(argv=None):
                    help="GroupGemm vs DenseGemm vs AUTO over the zipf token counts")
     p.add_argument("--pn-sweep", action="store_true",
                    help="step time over pipeline numbers and both stage kinds for --config")
+    p.add_argument("--pn-fit", action="store_true",
+                   help="fit the paper's pipeline overhead model R(N) = kN + b from serial "
+                        "stages of --config, choose PN with it and compare with the "
+                        "measured best PN")
+    p.add_argument("--cu-sweep", action="store_true",
+                   help="step time of --config over grouped-GEMM CU budgets and PN")
+    p.add_argument("--gemm-study", action="store_true",
+                   help="GroupGemm throughput over group counts, rows per group and CU "
+                        "budgets on the DeepSeekV2 expert shape")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                    help="only run a plain device copy of BYTES (HBM counter calibration)")
     return p.parse_args(argv)
@@ -123,7 +132,7 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_calibration_bytes": nbytes, "launches": 5}))
 
 
-def run_workload(args, shape, inp, steps, warmup, timing=True):
+def run_workload(args, shape, inp, steps, warmup, timing=True, serial=False, dev_inputs=None):
     import torch
 
     from paper_2410_12247_amd import moe
@@ -132,8 +141,9 @@ def run_workload(args, shape, inp, steps, warmup, timing=True):
     mode = {"auto": moe.GEMM_AUTO, "group": moe.GEMM_GROUP, "dense": moe.GEMM_DENSE}[args.mode]
     chunk = {"experts": moe.CHUNK_EXPERTS, "tokens": moe.CHUNK_TOKENS}[args.chunk_mode]
     o = moe.opts(gemm_mode=mode, pipeline_n=args.pn, gemm_cu_budget=args.cu_budget,
-                 dense_min_rows=args.dense_min_rows, timing=timing, chunk_mode=chunk)
-    g = DeviceInputs(inp)
+                 dense_min_rows=args.dense_min_rows, timing=timing, chunk_mode=chunk,
+                 serial=serial)
+    g = dev_inputs if dev_inputs is not None else DeviceInputs(inp)
     buf = g.buffers(o)
 
     def step():
@@ -218,6 +228,12 @@ def main(argv=None):
         return sweep(args)
     if args.pn_sweep:
         return pn_sweep(args)
+    if args.pn_fit:
+        return pn_fit(args)
+    if args.cu_sweep:
+        return cu_sweep(args)
+    if args.gemm_study:
+        return gemm_study(args)
     shape = synth.SHAPES[args.config]
     if args.tokens:
         shape = shape.with_tokens(args.tokens)
@@ -360,6 +376,144 @@ def pn_sweep(args):
                               "ms_per_step": round(wall_u / args.steps * 1e3, 4),
                               "phases_ms": {k: round(v, 4) for k, v in tm.items()
                                             if k.endswith("_ms")}}), flush=True)
+    return 0
+
+
+def _shape_of(args):
+    from paper_2410_12247_amd import synth
+
+    shape = synth.SHAPES[args.config]
+    return shape.with_tokens(args.tokens) if args.tokens else shape
+
+
+def pn_fit(args):
+    """The paper's pipeline-number model (Sec. 5.2) fitted on one GPU.  The
+    serial mode (every stage on one stream, nothing overlapped) gives the
+    cost of cutting the work into N expert-group stages, R(N) = T_serial(N)
+    - T_serial(1), fitted as kN + b by least squares; C = min(T_comm,
+    T_comp) from the unsplit forward's phases, with T_comm the one-GPU
+    stand-in for the dispatch and combine all2alls (gather + combine) and
+    T_comp the expert GEMMs.  moe_choose_pipeline_n picks PN from (C, k, b);
+    the measured best is the PN with the lowest pipelined step time."""
+    import numpy as np
+
+    from paper_2410_12247_amd import moe, synth
+    from paper_2410_12247_amd.workload import DeviceInputs
+
+    shape = _shape_of(args)
+    inp = synth.make_inputs(shape)
+    g = DeviceInputs(inp)
+    pns = [n for n in range(1, min(shape.EL, 20) + 1) if shape.EL % n == 0]
+    a1 = argparse.Namespace(**{**vars(args), "pn": 1, "chunk_mode": "experts"})
+    _, tms, _ = run_workload(a1, shape, inp, args.steps, args.warmup, timing=True, dev_inputs=g)
+    tm = summarize_timing(tms)
+    t_comm = tm["gather_ms"] + tm["combine_ms"]
+    t_comp = tm["gateup_ms"] + tm["down_ms"]
+    ser, pipe = {}, {}
+    for pn in pns:
+        a = argparse.Namespace(**{**vars(args), "pn": pn, "chunk_mode": "experts"})
+        w_s, _, _ = run_workload(a, shape, inp, args.steps, args.warmup, timing=False,
+                                 serial=True, dev_inputs=g)
+        w_p, _, _ = run_workload(a, shape, inp, args.steps, args.warmup, timing=False,
+                                 dev_inputs=g)
+        ser[pn] = w_s / args.steps * 1e3
+        pipe[pn] = w_p / args.steps * 1e3
+    n = np.array(pns, dtype=np.float64)
+    r = np.array([ser[p] - ser[1] for p in pns])
+    k, b = np.polyfit(n, r, 1) if len(pns) > 1 else (0.0, 0.0)
+    C = min(t_comm, t_comp)
+    chosen, gain = moe.choose_pipeline_n(C, max(k, 0.0), b, shape.EL)
+    best = min(pipe, key=pipe.get)
+    print(json.dumps({
+        "pn_fit": args.config, "tokens": shape.T, "local_experts": shape.EL,
+        "t_comm_ms": round(t_comm, 4), "t_comp_ms": round(t_comp, 4), "C_ms": round(C, 4),
+        "k_ms": round(float(k), 4), "b_ms": round(float(b), 4),
+        "serial_ms": {p: round(v, 4) for p, v in ser.items()},
+        "pipelined_ms": {p: round(v, 4) for p, v in pipe.items()},
+        "predicted_gain_ms": {p: round(C - b - (C / p + k * p), 4) for p in pns if p > 1},
+        "measured_gain_ms": {p: round(pipe[1] - pipe[p], 4) for p in pns if p > 1},
+        "chosen_pn": chosen, "chosen_gain_ms": round(gain, 4), "measured_best_pn": best,
+        "agree": chosen == best}), flush=True)
+    return 0
+
+
+def cu_sweep(args):
+    """Step time of --config over the grouped GEMM's persistent grid (its CU
+    budget: CUs left to the gather and combine of the other stages, the
+    paper's SM control, Sec. 5.2) and the pipeline number."""
+    from paper_2410_12247_amd import synth
+    from paper_2410_12247_amd.workload import DeviceInputs
+
+    shape = _shape_of(args)
+    inp = synth.make_inputs(shape)
+    g = DeviceInputs(inp)
+    for pn in [p for p in (1, 2, 4) if shape.EL % p == 0]:
+        for budget in (256, 248, 240, 224, 192, 160, 128):
+            a = argparse.Namespace(**{**vars(args), "pn": pn, "chunk_mode": "experts",
+                                      "cu_budget": budget})
+            w, _, _ = run_workload(a, shape, inp, args.steps, args.warmup, timing=False,
+                                   dev_inputs=g)
+            _, tms, _ = run_workload(a, shape, inp, PHASE_STEPS, 1, timing="gemm", dev_inputs=g)
+            tm = summarize_timing(tms)
+            print(json.dumps({"cu_sweep": args.config, "tokens": shape.T, "pipeline_n": pn,
+                              "gemm_cu_budget": budget,
+                              "ms_per_step": round(w / args.steps * 1e3, 4),
+                              "gateup_ms": round(tm["gateup_ms"], 4),
+                              "down_ms": round(tm["down_ms"], 4)}), flush=True)
+    return 0
+
+
+def gemm_study(args):
+    """GroupGemm (moe_ffn_group: gate/up + SiLU + down) on the DeepSeekV2
+    expert shape [1536, 5120], as in the paper's GEMM profiling (Sec. 3.2,
+    Conclusions 2 and 3): throughput over the group count at several rows
+    per group, relative to the best group count of the same rows (Fig. 4b),
+    and over the CU budget at 6144 rows per group (Fig. 4c).  Inputs are
+    seeded Gaussian bf16 tensors; the rows of each group are contiguous."""
+    import torch
+
+    from paper_2410_12247_amd import moe
+
+    H, I = 5120, 1536
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2410)
+
+    def normal(shape, sigma):
+        return (torch.randn(shape, generator=gen, device=dev) * sigma).to(torch.bfloat16)
+
+    GMAX, MMAX = 20, 6144
+    x = normal((GMAX * MMAX, H), 1.0)
+    wg, wu, wd = normal((GMAX, I, H), 0.02), normal((GMAX, I, H), 0.02), normal((GMAX, H, I), 0.02)
+    act = torch.empty((GMAX * MMAX, I), dtype=torch.bfloat16, device=dev)
+    y = torch.empty((GMAX * MMAX, H), dtype=torch.float32, device=dev)
+
+    def time_group(G, m, budget):
+        d = moe.dims(G * m, H, I, G, 1)
+        off = torch.arange(0, G * m + 1, m, dtype=torch.int32, device=dev)
+        run = lambda: moe.ffn_group(d, 0, G, off, x, wg, wu, wd, act, y, budget)  # noqa: E731
+        for _ in range(args.warmup):
+            run()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(args.steps):
+            run()
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / args.steps
+        return ms, 6.0 * G * m * H * I / (ms * 1e-3) / 1e12
+
+    for m in (128, 512, 2048, 6144):
+        res = {G: time_group(G, m, 0) for G in (1, 2, 4, 8, 16, 20)}
+        top = max(v[1] for v in res.values())
+        print(json.dumps({"gemm_study": "groups", "rows_per_group": m,
+                          "tflops": {G: round(v[1], 1) for G, v in res.items()},
+                          "relative": {G: round(v[1] / top, 3) for G, v in res.items()}}),
+              flush=True)
+    for G in (1, 4, 16):
+        res = {b: time_group(G, MMAX, b) for b in (256, 224, 192, 160, 128, 96, 64, 32)}
+        print(json.dumps({"gemm_study": "cu_budget", "groups": G, "rows_per_group": MMAX,
+                          "tflops": {b: round(v[1], 1) for b, v in res.items()}}), flush=True)
     return 0
 
 

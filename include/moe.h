@@ -71,7 +71,12 @@ typedef struct {
 
 enum { MOE_GEMM_AUTO = 0, MOE_GEMM_GROUP = 1, MOE_GEMM_DENSE = 2 };
 enum { MOE_CHUNK_EXPERTS = 0, MOE_CHUNK_TOKENS = 1 };
-enum { MOE_FLAG_TIMING = 1, MOE_FLAG_TIMING_GEMM = 2, MOE_FLAG_EXACT_ORDER = 4 };
+enum {
+    MOE_FLAG_TIMING = 1,
+    MOE_FLAG_TIMING_GEMM = 2,
+    MOE_FLAG_EXACT_ORDER = 4,
+    MOE_FLAG_SERIAL = 8
+};
 
 /* Options of moe_ffn_forward (Sec. 4.3 of the paper: the GroupGemm /
  * DenseGemm switch by load, the pipeline number PN and how the work is cut
@@ -106,7 +111,13 @@ typedef struct {
                                MOE_FLAG_EXACT_ORDER: no K split in the
                                grouped GEMM (see the determinism note at
                                the top); slower when the tile count leaves
-                               a partial last round of the grid. */
+                               a partial last round of the grid.
+                               MOE_FLAG_SERIAL: every step of every stage
+                               (and the shared experts) runs on the caller's
+                               stream in order, so nothing overlaps: the
+                               paper's serial mode (Sec. 5.2), which
+                               measures what cutting the work into PN stages
+                               costs by itself.  Same bits as without it. */
     int32_t chunk_mode;     /* MOE_CHUNK_EXPERTS or MOE_CHUNK_TOKENS */
     int32_t reserved[2];    /* must be zero */
 } moe_opts;
@@ -242,6 +253,20 @@ moe_status moe_last_timing(moe_timing *out);
  * dense_min_rows == 0.  On MI355X the grouped GEMM won at every measured
  * load, so the built-in value (2^30) is never reached. */
 int32_t moe_default_dense_min_rows(void);
+
+/* Pipeline number from the overhead model of the paper's ablation (Sec. 5.2):
+ * PN stages hide (PN - 1)/PN of C = min(T_comm, T_comp), the smaller of the
+ * unsplit communication and computation times, and cost R(PN) = k*PN + b, so
+ * the latency gain of PN > 1 is G(PN) = C - b - (C/PN + k*PN), largest near
+ * PN = sqrt(C/k).  Writes to *pn the PN in [1, local_count] that divides
+ * local_count and maximises G, with G(1) = 0 (no pipeline, no overhead); a
+ * pipeline is chosen only when its gain is positive, and ties go to the
+ * smaller PN.  k = 0 (no per-stage overhead) picks the largest PN whose gain
+ * is positive.  *gain_ms (may be NULL) receives G(*pn).  Times in ms; c_ms
+ * and k_ms must be finite and >= 0, b_ms finite, local_count in [1, 256],
+ * else MOE_ERR_INVALID.  Host-only; never touches the GPU. */
+moe_status moe_choose_pipeline_n(double c_ms, double k_ms, double b_ms, int32_t local_count,
+                                 int32_t *pn, double *gain_ms);
 
 const char *moe_status_string(moe_status s);
 const char *moe_last_error(void);

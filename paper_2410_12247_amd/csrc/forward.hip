@@ -18,6 +18,7 @@
 // is chosen from its row counts (GroupGemm for small loads, DenseGemm per
 // expert for large ones).
 #include <algorithm>
+#include <cmath>
 #include <mutex>
 #include <vector>
 
@@ -162,7 +163,8 @@ moe_status check_opts(const moe_dims *d, const moe_opts *o) {
         return fail(MOE_ERR_UNSUPPORTED, "token stages: pipeline_n * local_count > %d",
                     kMaxExperts);
     if (o->gemm_cu_budget < 0) return fail(MOE_ERR_INVALID, "gemm_cu_budget < 0");
-    if (o->flags & ~(MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM | MOE_FLAG_EXACT_ORDER))
+    if (o->flags &
+        ~(MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM | MOE_FLAG_EXACT_ORDER | MOE_FLAG_SERIAL))
         return fail(MOE_ERR_INVALID, "unknown flags 0x%x", o->flags);
     for (int i = 0; i < 2; ++i)
         if (o->reserved[i]) return fail(MOE_ERR_INVALID, "reserved options must be zero");
@@ -183,6 +185,37 @@ using namespace moe;
 extern "C" {
 
 int32_t moe_default_dense_min_rows(void) { return kDefaultDenseMinRows; }
+
+// The pipeline-number model of the paper's ablation (Sec. 5.2): the overlap
+// hides C/PN of each of PN - 1 stages, and cutting the work costs
+// k*PN + b, so G(PN) = C - b - (C/PN + k*PN) for PN > 1 and G(1) = 0.  The
+// candidates are the divisors of local_count (each stage an equal expert
+// group), searched exhaustively: the closed-form optimum sqrt(C/k) need not
+// be one of them.
+moe_status moe_choose_pipeline_n(double c_ms, double k_ms, double b_ms, int32_t local_count,
+                                 int32_t *pn, double *gain_ms) {
+    if (!pn) return fail(MOE_ERR_INVALID, "moe_choose_pipeline_n: NULL pn");
+    if (!std::isfinite(c_ms) || !std::isfinite(k_ms) || !std::isfinite(b_ms) || c_ms < 0 ||
+        k_ms < 0)
+        return fail(MOE_ERR_INVALID, "moe_choose_pipeline_n: C and k must be finite and >= 0, "
+                                     "b finite");
+    if (local_count < 1 || local_count > kMaxExperts)
+        return fail(MOE_ERR_INVALID, "moe_choose_pipeline_n: local_count %d out of range",
+                    local_count);
+    int32_t best = 1;
+    double best_gain = 0.0;
+    for (int32_t n = 2; n <= local_count; ++n) {
+        if (local_count % n) continue;
+        const double g = c_ms - b_ms - (c_ms / n + k_ms * n);
+        if (g > best_gain) {
+            best = n;
+            best_gain = g;
+        }
+    }
+    *pn = best;
+    if (gain_ms) *gain_ms = best_gain;
+    return MOE_OK;
+}
 
 moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe_bf16 *x,
                            const float *w_router, const float *bias,
@@ -247,9 +280,10 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     hipStream_t s0 = (hipStream_t)stream;
     // One stage without shared experts has nothing to overlap: every step
     // runs on the caller's stream (no cross-stream event hops, which cost
-    // tens of microseconds each).  Otherwise gather, GEMMs and combine run
-    // on their own streams so that stages (and the shared FFN) overlap.
-    const bool one_stream = PN == 1 && !has_shared;
+    // tens of microseconds each).  So does the serial mode, where nothing
+    // may overlap.  Otherwise gather, GEMMs and combine run on their own
+    // streams so that stages (and the shared FFN) overlap.
+    const bool one_stream = (PN == 1 && !has_shared) || (o->flags & MOE_FLAG_SERIAL) != 0;
     hipStream_t sg = one_stream ? s0 : st->sg;
     hipStream_t sm = one_stream ? s0 : st->sm;
     hipStream_t sc = one_stream ? s0 : st->sc;

@@ -18,12 +18,13 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmoe.so")
 
 GEMM_AUTO, GEMM_GROUP, GEMM_DENSE = 0, 1, 2
 CHUNK_EXPERTS, CHUNK_TOKENS = 0, 1
-FLAG_TIMING, FLAG_TIMING_GEMM, FLAG_EXACT_ORDER = 1, 2, 4
+FLAG_TIMING, FLAG_TIMING_GEMM, FLAG_EXACT_ORDER, FLAG_SERIAL = 1, 2, 4, 8
 
 # the entry points include/moe.h declares
 EXPORTS = ("moe_workspace_bytes", "moe_route", "moe_permute", "moe_gather", "moe_ffn_group",
            "moe_ffn_dense", "moe_combine", "moe_ffn_forward", "moe_last_timing",
-           "moe_default_dense_min_rows", "moe_status_string", "moe_last_error")
+           "moe_default_dense_min_rows", "moe_choose_pipeline_n", "moe_status_string",
+           "moe_last_error")
 
 
 class MoEError(RuntimeError):
@@ -80,11 +81,13 @@ def lib():
     L.moe_ffn_forward.argtypes = [D, O, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
     L.moe_last_timing.argtypes = [ctypes.POINTER(Timing)]
     L.moe_default_dense_min_rows.restype = I32
+    L.moe_choose_pipeline_n.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double, I32,
+                                        ctypes.POINTER(I32), ctypes.POINTER(ctypes.c_double)]
     L.moe_status_string.argtypes = [I32]
     L.moe_status_string.restype = ctypes.c_char_p
     L.moe_last_error.restype = ctypes.c_char_p
     for name in ("moe_route", "moe_permute", "moe_gather", "moe_ffn_group", "moe_ffn_dense",
-                 "moe_combine", "moe_ffn_forward", "moe_last_timing"):
+                 "moe_combine", "moe_ffn_forward", "moe_last_timing", "moe_choose_pipeline_n"):
         getattr(L, name).restype = I32
     _lib = L
     return L
@@ -105,16 +108,19 @@ def dims(tokens, hidden, inter, experts, top_k, local_begin=0, local_count=None,
 
 
 def opts(gemm_mode=GEMM_AUTO, dense_min_rows=0, pipeline_n=1, gemm_cu_budget=0,
-         timing=False, chunk_mode=CHUNK_EXPERTS, exact_order=False) -> Opts:
+         timing=False, chunk_mode=CHUNK_EXPERTS, exact_order=False, serial=False) -> Opts:
     """timing: False, True (every phase) or "gemm" (the GEMM launches only).
     exact_order: no K split of the grouped GEMM's last round (the same bits
-    for every pipeline number, stage kind, CU budget and GEMM kind)."""
+    for every pipeline number, stage kind, CU budget and GEMM kind).
+    serial: every stage on the caller's stream, nothing overlapped."""
     o = Opts()
     o.gemm_mode, o.dense_min_rows, o.pipeline_n = gemm_mode, dense_min_rows, pipeline_n
     o.gemm_cu_budget = gemm_cu_budget
     o.flags = FLAG_TIMING_GEMM if timing == "gemm" else (FLAG_TIMING if timing else 0)
     if exact_order:
         o.flags |= FLAG_EXACT_ORDER
+    if serial:
+        o.flags |= FLAG_SERIAL
     o.chunk_mode = chunk_mode
     return o
 
@@ -177,6 +183,15 @@ def forward(d, o, x, w_router, bias, w_gate, w_up, w_down, shared_gate, shared_u
                                  _p(w_down), _p(shared_gate), _p(shared_up), _p(shared_down),
                                  _p(y), _p(topk_ids), _p(topk_w), _p(counts), _p(ws),
                                  ws.numel() * ws.element_size(), _s(stream)))
+
+
+def choose_pipeline_n(c_ms: float, k_ms: float, b_ms: float, local_count: int):
+    """(PN, gain in ms) from the paper's pipeline overhead model."""
+    pn = ctypes.c_int32()
+    gain = ctypes.c_double()
+    _check(lib().moe_choose_pipeline_n(float(c_ms), float(k_ms), float(b_ms), int(local_count),
+                                       ctypes.byref(pn), ctypes.byref(gain)))
+    return pn.value, gain.value
 
 
 def last_timing() -> dict:

@@ -104,7 +104,7 @@ def test_invalid_options_and_buffers_rejected():
                            None, None, None, fake, None, None, None, fake, 1 << 40, None)
     assert st == 1
     o = moe.opts()
-    o.flags = 8  # unknown flag
+    o.flags = 16  # unknown flag
     st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake, fake,
                            None, None, None, fake, None, None, None, fake, 1 << 40, None)
     assert st == 1
@@ -145,3 +145,42 @@ def test_zero_token_calls_are_noops_on_the_host():
     assert L.moe_permute(ctypes.byref(d), None, None, None, None, None, None, None, None, 0,
                          None) == 0
     assert L.moe_ffn_dense(0, 256, 128, None, None, None, None, None, None, None) == 0
+
+
+def test_pipeline_n_chooser_model():
+    """moe_choose_pipeline_n against the properties of the paper's pipeline
+    model (Sec. 5.2): gain C(1 - 1/N) - (kN + b), best near sqrt(C/k),
+    bounded by C - b - 2 sqrt(kC), only divisors of the local expert count,
+    no pipeline unless it gains."""
+    ch = moe.choose_pipeline_n
+    # sqrt(C/k) = 4 divides 20: the closed form, with the bound reached
+    pn, g = ch(16.0, 1.0, 0.0, 20)
+    assert pn == 4 and g == pytest.approx(16 - 2 * (16 * 1.0) ** 0.5)
+    # sqrt(9) = 3 does not divide 20: the better neighbour among 2, 4, 5
+    # (gains 2.5, 2.75, 2.2)
+    pn, g = ch(9.0, 1.0, 0.0, 20)
+    assert pn == 4 and g == pytest.approx(2.75)
+    # no per-stage overhead: the more stages, the better
+    assert ch(5.0, 0.0, 0.0, 20)[0] == 20
+    assert ch(5.0, 0.0, 0.0, 7)[0] == 7
+    # a fixed overhead above every gain keeps one stage
+    assert ch(16.0, 1.0, 10.0, 20) == (1, 0.0)
+    # nothing to hide, one expert, or a prime count with a steep overhead
+    assert ch(0.0, 0.1, 0.0, 8) == (1, 0.0)
+    assert ch(16.0, 0.1, 0.0, 1) == (1, 0.0)
+    assert ch(1.0, 1.0, 0.0, 7) == (1, 0.0)
+    # the gain never exceeds the paper's bound and is the best divisor's
+    for C, k, b, EL in [(3.0, 0.05, 0.1, 20), (0.14, 0.1, 0.0, 8), (2.0, 0.3, -0.2, 16),
+                        (40.0, 0.01, 1.0, 160)]:
+        pn, g = ch(C, k, b, EL)
+        assert EL % pn == 0
+        if pn > 1:
+            assert g <= C - b - 2 * (k * C) ** 0.5 + 1e-12
+        gains = {n: C - b - (C / n + k * n) for n in range(2, EL + 1) if EL % n == 0}
+        assert g == pytest.approx(max([0.0] + list(gains.values())))
+    # invalid arguments
+    for args in [(float("nan"), 1.0, 0.0, 8), (-1.0, 1.0, 0.0, 8), (1.0, -1.0, 0.0, 8),
+                 (1.0, 1.0, float("inf"), 8), (1.0, 1.0, 0.0, 0), (1.0, 1.0, 0.0, 257)]:
+        with pytest.raises(moe.MoEError) as e:
+            ch(*args)
+        assert e.value.status == 1

@@ -203,8 +203,8 @@ def test_forward(name):
 
 @pytest.mark.parametrize("name", ["ragged8", "fine"])
 def test_forward_invariant_to_pipeline_and_gemm_kind(name):
-    """With MOE_FLAG_EXACT_ORDER, PN, the GEMM kind, the CU budget and a
-    repeated call all give the same bits."""
+    """With MOE_FLAG_EXACT_ORDER, PN, the GEMM kind, the CU budget, serial
+    stages and a repeated call all give the same bits."""
     inp, _, _ = case(name)
     g = Dev(inp)
     EL = inp.shape.EL
@@ -213,6 +213,8 @@ def test_forward_invariant_to_pipeline_and_gemm_kind(name):
         for mode in (moe.GEMM_GROUP, moe.GEMM_DENSE, moe.GEMM_AUTO):
             y = g.forward(moe.opts(gemm_mode=mode, pipeline_n=pn, exact_order=True)).y
             assert torch.equal(y, base), f"PN={pn} mode={mode} differs"
+        y = g.forward(moe.opts(pipeline_n=pn, exact_order=True, serial=True)).y
+        assert torch.equal(y, base), f"serial PN={pn} differs"
     y = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP, gemm_cu_budget=40, exact_order=True)).y
     assert torch.equal(y, base), "CU budget changes the bits"
 

@@ -90,6 +90,7 @@ WsLayout ws_layout(const moe_dims *d, bool forward, int nbuckets) {
         L.act = take(sizeof(bf16_t) * L.rcap * d->inter);
         L.y_perm = take(sizeof(float) * L.rcap * d->hidden);
         L.shared_act = take(sizeof(bf16_t) * T * d->shared_inter);
+        L.shared_off = take(sizeof(int32_t) * 2);
         L.split_part = take(gemm_split_bytes());
         L.split_meta = take(sizeof(int32_t) * kSplitMetaInts);
     }

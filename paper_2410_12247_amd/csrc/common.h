@@ -63,6 +63,7 @@ struct WsLayout {
     size_t act;           // bf16  [Rcap][I]
     size_t y_perm;        // fp32  [Rcap][H]
     size_t shared_act;    // bf16  [T][Is]
+    size_t shared_off;    // int32 [2] = {0, T}: the shared FFN as one grouped-GEMM expert
     size_t split_part;    // fp32  grouped-GEMM K-split partials (gemm_split_bytes)
     size_t split_meta;    // int32 [kSplitMetaInts] K-split tail-tile records
     size_t total;

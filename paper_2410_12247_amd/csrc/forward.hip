@@ -27,6 +27,12 @@
 namespace moe {
 namespace {
 
+// Row offsets {0, T} of the shared FFN run as one grouped-GEMM expert
+// (vector stores from two lanes).
+__global__ void shared_offsets_kernel(int32_t *__restrict__ off, int32_t T) {
+    if (threadIdx.x < 2) off[threadIdx.x] = threadIdx.x == 0 ? 0 : T;
+}
+
 // AUTO's DenseGemm threshold (rows of every expert of a stage).  Measured on
 // MI355X over the skewed DeepSeekV2-shaped sweep (T = 64 .. 65536, up to
 // 58K rows on one expert) and the Mixtral / DBRX shards, the grouped launch
@@ -298,11 +304,30 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
         MOE_HIP(hipStreamWaitEvent(sm, ev_start, 0));
         tm.gap();
     }
+    // persistent grid of the grouped GEMMs and their K-split scratch (all
+    // on the GEMM stream, one GEMM after another)
+    int grid = o->gemm_cu_budget > 0 ? o->gemm_cu_budget : device_cu_count();
+    grid = std::max(8, (grid / 8) * 8);
+    const bool split = (o->flags & MOE_FLAG_EXACT_ORDER) == 0;
+    float *split_part = split ? reinterpret_cast<float *>(base + L.split_part) : nullptr;
+    int32_t *split_meta = split ? reinterpret_cast<int32_t *>(base + L.split_meta) : nullptr;
     if (has_shared) {
+        // the shared FFN is one expert of T contiguous rows through the
+        // grouped scheduler, whose K split shortens a partial last round of
+        // tiles (e.g. 1040 down tiles on 256 workgroups); same tile code, so
+        // the same bits as a dense launch under MOE_FLAG_EXACT_ORDER
+        moe_dims ds = d;
+        ds.inter = d.shared_inter;
+        ds.local_begin = 0;
+        ds.local_count = 1;
+        int32_t *soff = reinterpret_cast<int32_t *>(base + L.shared_off);
         MOE_TRY(tm.begin(sm, PH_SHARED));
-        MOE_HIP(launch_dense_gateup(T, H, d.shared_inter, x, shared_gate, shared_up, shared_act,
-                                    sm));
-        MOE_HIP(launch_dense_down(T, H, d.shared_inter, shared_act, shared_down, y, sm));
+        shared_offsets_kernel<<<1, 64, 0, sm>>>(soff, (int32_t)T);
+        MOE_HIP(hipGetLastError());
+        MOE_HIP(launch_group_gateup(ds, 0, 1, soff, x, nullptr, shared_gate, shared_up,
+                                    shared_act, grid, split_part, split_meta, sm));
+        MOE_HIP(launch_group_down(ds, 0, 1, soff, shared_act, shared_down, y, grid, split_part,
+                                  split_meta, sm));
         MOE_TRY(tm.end(sm));
     }
 
@@ -313,11 +338,6 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     MOE_TRY(tm.end(s0));
     MOE_TRY(tm.begin(s0, PH_PERMUTE));
     MOE_HIP(launch_permute(d, ids, ws, L, tps, cnt, off, cnt_el, sorted_slot, slot_row, s0));
-    // K-split scratch of the grouped GEMMs (all on the GEMM stream, one
-    // after another)
-    const bool split = (o->flags & MOE_FLAG_EXACT_ORDER) == 0;
-    float *split_part = split ? reinterpret_cast<float *>(base + L.split_part) : nullptr;
-    int32_t *split_meta = split ? reinterpret_cast<int32_t *>(base + L.split_meta) : nullptr;
     MOE_TRY(tm.end(s0));
 
     // GEMM kind per stage needs the row counts on the host
@@ -340,8 +360,6 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     // the grouped gate/up GEMM can gather its token rows itself while every
     // byte offset into x fits 32 bits
     const bool fold_ok = (uint64_t)T * (uint64_t)H * 2u < (uint64_t(1) << 32);
-    int grid = o->gemm_cu_budget > 0 ? o->gemm_cu_budget : device_cu_count();
-    grid = std::max(8, (grid / 8) * 8);
 
     if (!one_stream) {
         MOE_HIP(hipEventRecord(ev_fork, s0));

@@ -178,9 +178,11 @@ def measured_traffic(workload, kernel_prefix):
     src = open(os.path.join(ROOT, "paper_2410_12247_amd", "csrc", "gemm.hip"), "rb").read()
     if d.get("gemm_source_sha256") != hashlib.sha256(src).hexdigest():
         return None
-    for k, v in d["kernels"].items():
-        if k.startswith(kernel_prefix):
-            return v["bytes"]
+    # with shared experts the summary lists the routed launch separately
+    keys = [k for k in d["kernels"] if k.startswith(kernel_prefix)]
+    routed = [k for k in keys if k.endswith("(routed)")]
+    for k in routed or keys:
+        return d["kernels"][k]["bytes"]
     return None
 
 

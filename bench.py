@@ -470,8 +470,10 @@ def gemm_study(args):
     expert shape [1536, 5120], as in the paper's GEMM profiling (Sec. 3.2,
     Conclusions 2 and 3): throughput over the group count at several rows
     per group, relative to the best group count of the same rows (Fig. 4b),
-    and over the CU budget at 6144 rows per group (Fig. 4c).  Inputs are
-    seeded Gaussian bf16 tensors; the rows of each group are contiguous."""
+    and over the CU budget at 6144 rows per group (Fig. 4c); then GroupGemm
+    against one DenseGemm launch per expert at uniform load, 16 experts of m
+    rows each (Fig. 4a).  Inputs are seeded Gaussian bf16 tensors; the rows of
+    each group are contiguous."""
     import torch
 
     from paper_2410_12247_amd import moe
@@ -516,6 +518,32 @@ def gemm_study(args):
         res = {b: time_group(G, MMAX, b) for b in (256, 224, 192, 160, 128, 96, 64, 32)}
         print(json.dumps({"gemm_study": "cu_budget", "groups": G, "rows_per_group": MMAX,
                           "tflops": {b: round(v[1], 1) for b, v in res.items()}}), flush=True)
+
+    # GroupGemm vs DenseGemm at uniform load (Fig. 4a): 16 experts of m rows
+    # each as one grouped launch, or as one dense launch per expert
+    def time_dense(G, m):
+        def run():
+            for e in range(G):
+                r = slice(e * m, (e + 1) * m)
+                moe.ffn_dense(m, H, I, x[r], wg[e], wu[e], wd[e], act[r], y[r])
+        for _ in range(args.warmup):
+            run()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(args.steps):
+            run()
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / args.steps
+        return ms, 6.0 * G * m * H * I / (ms * 1e-3) / 1e12
+
+    for m in (128, 512, 1024, 2048, 4096, 6144):
+        g_ms, g_tf = time_group(16, m, 0)
+        d_ms, d_tf = time_dense(16, m)
+        print(json.dumps({"gemm_study": "group_vs_dense", "experts": 16, "rows_per_expert": m,
+                          "group_ms": round(g_ms, 4), "dense_ms": round(d_ms, 4),
+                          "group_tflops": round(g_tf, 1), "dense_tflops": round(d_tf, 1)}),
+              flush=True)
     return 0
 
 

@@ -37,13 +37,17 @@ CASES = {
 # grid with K long enough to be cut (pieces of at least 32 K stages of 32):
 # split2 cuts both GEMMs in 2 (K = 2048), split3 the down GEMM in 3
 # (K = 3072, ragged experts in a local window), split4 and split8 the
-# gate/up GEMM in 4 and 8 (K = 4096 and 8192, few rows per expert).
+# gate/up GEMM in 4 and 8 (K = 4096 and 8192, few rows per expert);
+# split_shared runs the shared FFN (width 2048) as one grouped expert of all
+# T rows, whose down GEMM (one tile, K = 2048) is cut in 2.
 SPLIT_CASES = {
     "split2": C(name="split2", index=210, T=300, H=2048, I=2048, E=8, EL=8, k=2, renorm=True),
     "split3": C(name="split3", index=212, T=250, H=320, I=3072, E=16, EL=6, e0=5, k=4,
                 renorm=False),
     "split4": C(name="split4", index=211, T=64, H=4096, I=512, E=8, EL=8, k=2, renorm=True),
     "split8": C(name="split8", index=213, T=32, H=8192, I=256, E=8, EL=8, k=2, renorm=True),
+    "split_shared": C(name="split_shared", index=215, T=300, H=256, I=128, E=8, EL=8, k=2,
+                      renorm=True, n_shared=1, Is=2048),
 }
 CASES.update(SPLIT_CASES)
 
@@ -282,7 +286,7 @@ def test_forward_k_split(name):
     # where the fp32 down GEMM is cut, the pieces' sums differ from one pass
     # in the last bits somewhere (the evidence that the split ran; a cut
     # gate/up shows only through rare bf16 rounding flips of act)
-    if name in ("split2", "split3"):
+    if name in ("split2", "split3", "split_shared"):
         assert not torch.equal(y, ye), "no tile was split"
     assert_close(y.cpu().numpy(), ye.cpu().numpy().astype(np.float64), f"{name} split vs exact",
                  max_abs=2e-3, rel_fro=1e-4)

@@ -7,8 +7,10 @@
 //
 // One wave per token: the wave reads the token's k slot records, orders the
 // selected ones by expert id (each ranked by counting smaller ids), then streams
-// the hidden dimension in 16-byte vectors, four per lane per pass so that all
-// loads of a pass are in flight together.
+// the hidden dimension in 16-byte vectors, four per lane per pass; a pass
+// issues the loads of all of the token's rows before its first fma, so the
+// rows' loads are in flight together (KS, the most rows a token can have
+// here, bounds the registers this takes).
 #include "common.h"
 
 namespace moe {
@@ -24,6 +26,7 @@ __device__ __forceinline__ void store_stream(float4 *p, float4 v) {
     __builtin_nontemporal_store(__builtin_bit_cast(floatx4, v), reinterpret_cast<floatx4 *>(p));
 }
 
+template <int KS>
 __global__ __launch_bounds__(256) void combine_kernel(int64_t t_begin, int64_t t_end, int H,
                                                       int k, int e0,
                                                       int e_lo, int e_hi,
@@ -92,21 +95,28 @@ __global__ __launch_bounds__(256) void combine_kernel(int64_t t_begin, int64_t t
             const int v = min(v0 + 64 * u, vecs - 1);
             acc[u] = accumulate ? load_stream(yrow + v) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
+        // every row's loads first, then the fmas in ascending expert order
+        float4 p[KS][4];
 #pragma unroll
-        for (int j = 0; j < kMaxTopK; ++j) {
+        for (int j = 0; j < KS; ++j) {
             if (j < n) {
                 const float4 *prow =
                     reinterpret_cast<const float4 *>(y_perm + (int64_t)orow[j] * H);
-                const float c = ow[j];
-                float4 p[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) p[u] = load_stream(prow + min(v0 + 64 * u, vecs - 1));
+                for (int u = 0; u < 4; ++u)
+                    p[j][u] = load_stream(prow + min(v0 + 64 * u, vecs - 1));
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < KS; ++j) {
+            if (j < n) {
+                const float c = ow[j];
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
-                    acc[u].x = __builtin_fmaf(c, p[u].x, acc[u].x);
-                    acc[u].y = __builtin_fmaf(c, p[u].y, acc[u].y);
-                    acc[u].z = __builtin_fmaf(c, p[u].z, acc[u].z);
-                    acc[u].w = __builtin_fmaf(c, p[u].w, acc[u].w);
+                    acc[u].x = __builtin_fmaf(c, p[j][u].x, acc[u].x);
+                    acc[u].y = __builtin_fmaf(c, p[j][u].y, acc[u].y);
+                    acc[u].z = __builtin_fmaf(c, p[j][u].z, acc[u].z);
+                    acc[u].w = __builtin_fmaf(c, p[j][u].w, acc[u].w);
                 }
             }
         }
@@ -124,10 +134,18 @@ hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, int64_t t
                           hipStream_t s) {
     if (t_end <= t_begin) return hipSuccess;
     const int64_t blocks = (t_end - t_begin + 3) / 4;
-    combine_kernel<<<(unsigned)blocks, 256, 0, s>>>(t_begin, t_end, d.hidden, d.top_k,
-                                                    d.local_begin, e_first, e_first + e_count,
-                                                    y_perm, ids, slot_row, w, y, accumulate);
-    return hipGetLastError();
+    // a token has at most k rows in range
+    const int ks = d.top_k;
+    auto go = [&](auto kernel) {
+        kernel<<<(unsigned)blocks, 256, 0, s>>>(t_begin, t_end, d.hidden, d.top_k, d.local_begin,
+                                                e_first, e_first + e_count, y_perm, ids,
+                                                slot_row, w, y, accumulate);
+        return hipGetLastError();
+    };
+    if (ks <= 1) return go(combine_kernel<1>);
+    if (ks <= 2) return go(combine_kernel<2>);
+    if (ks <= 4) return go(combine_kernel<4>);
+    return go(combine_kernel<kMaxTopK>);
 }
 
 }  // namespace moe

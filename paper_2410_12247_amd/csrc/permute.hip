@@ -92,7 +92,21 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t *__restrict__ c
     const int e = threadIdx.x;
     int run = 0;
     if (e < NB) {
-        for (int64_t c = 0; c < nchunks; ++c) {
+        // sixteen chunks' counts loaded before they are summed, so a long
+        // chunk list costs nchunks / 16 memory round trips, not nchunks
+        constexpr int U = 16;
+        int64_t c = 0;
+        for (; c + U <= nchunks; c += U) {
+            int v[U];
+#pragma unroll
+            for (int i = 0; i < U; ++i) v[i] = chunk_counts[(c + i) * NB + e];
+#pragma unroll
+            for (int i = 0; i < U; ++i) {
+                chunk_base[(c + i) * NB + e] = run;
+                run += v[i];
+            }
+        }
+        for (; c < nchunks; ++c) {
             const int v = chunk_counts[c * NB + e];
             chunk_base[c * NB + e] = run;
             run += v;

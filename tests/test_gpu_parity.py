@@ -86,6 +86,25 @@ def test_route(name):
     assert weights_match(gw.cpu().numpy(), w)
 
 
+@pytest.mark.parametrize("T,E", [(4000, 160), (8192, 160), (12001, 130), (16384, 160),
+                                 (20000, 150)])
+def test_route_many_experts_token_tiles(T, E):
+    """The register-tiled router for 129-160 experts takes 1, 2 or 4 tokens
+    per thread by batch size (below 8192, below 16384, from 16384): every band,
+    ragged T and E not a multiple of the 32 expert groups, against the oracle
+    bit for bit."""
+    shp = C(name=f"tiles{T}_{E}", index=216, T=T, H=128, I=64, E=E, EL=4, k=6, renorm=False)
+    inp = synth.make_inputs(shp, router_only=True)
+    _, ids, w = oracle.route(inp.x, inp.w_router, None, shp.k, shp.renorm)
+    d = moe.dims(T, shp.H, shp.I, E, shp.k, 0, shp.EL, False)
+    gids = torch.empty((T, shp.k), dtype=torch.int32, device=dev())
+    gw = torch.empty((T, shp.k), dtype=torch.float32, device=dev())
+    moe.route(d, bf16(inp.x), f32(inp.w_router), None, gids, gw)
+    torch.cuda.synchronize()
+    assert np.array_equal(gids.cpu().numpy(), ids)
+    assert weights_match(gw.cpu().numpy(), w)
+
+
 def test_route_ties_and_signed_zero():
     """Exact ties in the logits (duplicated router rows, zero rows) must go to
     the lower expert index, -0 and +0 being equal."""

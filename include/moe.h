@@ -203,8 +203,10 @@ moe_status moe_ffn_group(const moe_dims *dims, int32_t e_first, int32_t e_count,
  *   act[r] = bf16(silu(w_gate x[r]) * (w_up x[r])),  y[r] = w_down act[r]
  * x [rows][hidden] bf16; w_gate, w_up [inter][hidden]; w_down
  * [hidden][inter]; act [rows][inter] bf16 scratch; y [rows][hidden] fp32.
- * Also used for the shared experts (inter = shared width, x = all tokens).
- * Same arithmetic and bits as moe_ffn_group for the same rows. */
+ * Usable for shared experts (inter = shared width, x = all tokens), which
+ * moe_ffn_forward runs through the grouped scheduler instead (one expert
+ * of T rows).  Same arithmetic and bits as moe_ffn_group for the same
+ * rows. */
 moe_status moe_ffn_dense(int64_t rows, int32_t hidden, int32_t inter, const moe_bf16 *x,
                          const moe_bf16 *w_gate, const moe_bf16 *w_up,
                          const moe_bf16 *w_down, moe_bf16 *act, float *y, void *stream);
@@ -229,7 +231,8 @@ moe_status moe_combine(const moe_dims *dims, int32_t e_first, int32_t e_count,
  * Sec. 4.3) ; combine }, with stage i+1's gather and stage i-1's combine
  * running on their own streams beside stage i's GEMMs (the one-GPU form of
  * the expert pipeline of Sec. 4.3-4.4).  The shared experts (if any) run
- * first and write y; otherwise the first combine writes every token.
+ * first, as one grouped-GEMM expert of all T rows, and write y; otherwise
+ * the first combine writes every token.
  * topk_ids, topk_w, counts: optional outputs (NULL = keep them in the
  * workspace).  shared_*: required iff dims->shared_inter > 0.
  * ws: at least moe_workspace_bytes(dims, opts) bytes of device memory.

@@ -105,6 +105,30 @@ def test_route_many_experts_token_tiles(T, E):
     assert weights_match(gw.cpu().numpy(), w)
 
 
+@pytest.mark.parametrize("T,E,k", [(777, 256, 8), (2500, 256, 8), (1500, 200, 7)])
+def test_maximum_experts_and_top_k(T, E, k):
+    """The supported maximum, 256 experts with top-8 (and a ragged 200 with
+    top-7): the router alone (16 experts per thread) and the whole forward
+    (the streaming router up to 1024 tokens, the combine of eight slots)
+    against the oracle."""
+    shp = C(name=f"max{T}_{E}", index=217, T=T, H=192, I=128, E=E, EL=32, e0=E - 40, k=k,
+            renorm=True)
+    inp = synth.make_inputs(shp)
+    _, ids, w = oracle.route(inp.x, inp.w_router, None, k, True)
+    g = Dev(inp)
+    gids = torch.empty((T, k), dtype=torch.int32, device=dev())
+    gw = torch.empty((T, k), dtype=torch.float32, device=dev())
+    moe.route(g.d, g.x, g.w_router, g.bias, gids, gw)
+    torch.cuda.synchronize()
+    assert np.array_equal(gids.cpu().numpy(), ids)
+    assert weights_match(gw.cpu().numpy(), w)
+    buf = g.forward()
+    assert np.array_equal(buf.topk_ids.cpu().numpy(), ids)
+    counts, *_ = oracle.dispatch(ids, shp.e0, shp.EL)
+    assert np.array_equal(buf.counts.cpu().numpy(), counts)
+    assert_close(buf.y.cpu().numpy(), oracle_y(inp, ids, w, np.arange(T)), f"E={E} k={k}")
+
+
 def test_route_ties_and_signed_zero():
     """Exact ties in the logits (duplicated router rows, zero rows) must go to
     the lower expert index, -0 and +0 being equal."""

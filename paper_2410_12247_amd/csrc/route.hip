@@ -310,6 +310,35 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
     }
 }
 
+// Half a stage's operands of the streaming router, read together with one
+// wait: this thread's four 16-byte x chunks and its expert's 32 router
+// weights (eight 16-byte reads from one base).  Written out because the
+// compiler puts a full vmcnt(0) in front of LDS reads that may alias the
+// LDS-DMA requests in flight, which drains the ring every stage; the ring's
+// own vmcnt wait and barrier order the data (the slot read here landed for
+// every wave before the barrier, and is refilled only after the next one).
+__device__ __forceinline__ void stream_half_operands(u32x4 (&v)[4], floatx4 (&w)[8],
+                                                     const uint32_t (&a)[4], uint32_t wa) {
+    asm volatile(
+        "ds_read_b128 %0, %12\n\t"
+        "ds_read_b128 %1, %13\n\t"
+        "ds_read_b128 %2, %14\n\t"
+        "ds_read_b128 %3, %15\n\t"
+        "ds_read_b128 %4, %16\n\t"
+        "ds_read_b128 %5, %16 offset:16\n\t"
+        "ds_read_b128 %6, %16 offset:32\n\t"
+        "ds_read_b128 %7, %16 offset:48\n\t"
+        "ds_read_b128 %8, %16 offset:64\n\t"
+        "ds_read_b128 %9, %16 offset:80\n\t"
+        "ds_read_b128 %10, %16 offset:96\n\t"
+        "ds_read_b128 %11, %16 offset:112\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(w[0]), "=&v"(w[1]),
+          "=&v"(w[2]), "=&v"(w[3]), "=&v"(w[4]), "=&v"(w[5]), "=&v"(w[6]), "=&v"(w[7])
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(wa)
+        : "memory");
+}
+
 // Streaming router: workgroup = TB tokens x EB experts (TB * EB = 256), one
 // fma chain per thread.  x rows (bf16) and router rows (fp32) stream through
 // an LDS ring of RS_NS stages of RS_HS h by LDS-DMA, RS_NS - 1 stages in
@@ -322,13 +351,14 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
 // The logits go to z [T][E] and route_select_kernel picks.  (A fused form
 // for E <= 16, the workgroup picking the top-k of its tokens itself, was
 // slower than route_kernel at every T.)
-constexpr int RS_HS = 64;  // h per stage
+constexpr int RS_HS = 64;  // h per stage (two halves of four 16-byte x chunks)
 constexpr int RS_NS = 8;   // stages in the ring
 template <int TB, int EB>
 __global__ __launch_bounds__(RT_THREADS) void route_stream_kernel(
     const bf16_t *__restrict__ x, const float *__restrict__ wr, const float *__restrict__ bias,
     int64_t T, int H, int E, float *__restrict__ z) {
     static_assert(TB * EB == RT_THREADS, "one chain per thread");
+    static_assert(RS_HS == 64, "stage reads: 8 x chunks of 8 h, 2 x 32 weights");
     constexpr int XB = TB * RS_HS * 2;    // bytes of an x stage
     constexpr int WB = EB * RS_HS * 4;    // bytes of a router stage
     constexpr int NXI = XB / 1024;        // wave-wide 16-byte DMA requests
@@ -385,6 +415,13 @@ __global__ __launch_bounds__(RT_THREADS) void route_stream_kernel(
 #pragma unroll
     for (int st = 0; st < RS_NS - 1; ++st)
         if (st < nst) issue(st);
+    // LDS byte addresses in ring slot 0: chunk c of this thread's x row
+    // (stored at c ^ (row % 8)), and its expert's router row
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void_t *)lds;
+    uint32_t xaddr[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) xaddr[c] = lds0 + tb * (RS_HS * 2) + ((c ^ (tb & 7)) * 16);
+    const uint32_t waddr = lds0 + XB + eb * (RS_HS * 4);
     float acc = 0.0f;
     for (int st = 0; st < nst; ++st) {
         // stage st landed (this wave's share; later stages may be in flight)
@@ -398,22 +435,28 @@ __global__ __launch_bounds__(RT_THREADS) void route_stream_kernel(
         // a fenced barrier would drain the requests still in flight)
         __builtin_amdgcn_s_barrier();
         if (st + RS_NS - 1 < nst) issue(st + RS_NS - 1);
-        const char *slot = lds + (st % RS_NS) * STAGE;
-        const char *xr = slot + tb * (RS_HS * 2);
-        const float *wrow = reinterpret_cast<const float *>(slot + XB) + eb * RS_HS;
+        const uint32_t sbase = (uint32_t)((st % RS_NS) * STAGE);
 #pragma unroll
-        for (int c = 0; c < RS_HS / 8; ++c) {
-            const uint4 xv = *reinterpret_cast<const uint4 *>(xr + ((c ^ (tb & 7)) * 16));
-            const float4 w0 = *reinterpret_cast<const float4 *>(wrow + c * 8);
-            const float4 w1 = *reinterpret_cast<const float4 *>(wrow + c * 8 + 4);
-            acc = __builtin_fmaf(bf16_lo(xv.x), w0.x, acc);
-            acc = __builtin_fmaf(bf16_hi(xv.x), w0.y, acc);
-            acc = __builtin_fmaf(bf16_lo(xv.y), w0.z, acc);
-            acc = __builtin_fmaf(bf16_hi(xv.y), w0.w, acc);
-            acc = __builtin_fmaf(bf16_lo(xv.z), w1.x, acc);
-            acc = __builtin_fmaf(bf16_hi(xv.z), w1.y, acc);
-            acc = __builtin_fmaf(bf16_lo(xv.w), w1.z, acc);
-            acc = __builtin_fmaf(bf16_hi(xv.w), w1.w, acc);
+        for (int half = 0; half < 2; ++half) {
+            uint32_t a[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a[i] = xaddr[half * 4 + i] + sbase;
+            u32x4 xs[4];
+            floatx4 ws[8];
+            stream_half_operands(xs, ws, a, waddr + sbase + half * 128);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const u32x4 xv = xs[i];
+                const floatx4 w0 = ws[2 * i], w1 = ws[2 * i + 1];
+                acc = __builtin_fmaf(bf16_lo(xv.x), w0.x, acc);
+                acc = __builtin_fmaf(bf16_hi(xv.x), w0.y, acc);
+                acc = __builtin_fmaf(bf16_lo(xv.y), w0.z, acc);
+                acc = __builtin_fmaf(bf16_hi(xv.y), w0.w, acc);
+                acc = __builtin_fmaf(bf16_lo(xv.z), w1.x, acc);
+                acc = __builtin_fmaf(bf16_hi(xv.z), w1.y, acc);
+                acc = __builtin_fmaf(bf16_lo(xv.w), w1.z, acc);
+                acc = __builtin_fmaf(bf16_hi(xv.w), w1.w, acc);
+            }
         }
     }
     const int e = e0 + eb;

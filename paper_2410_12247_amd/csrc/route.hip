@@ -148,6 +148,19 @@ __device__ __forceinline__ void select_token(const float *zrow, int64_t t, int E
     }
 }
 
+// One 16-byte-per-lane LDS-DMA request (lane l's bytes land at lds_addr +
+// 16 l; lds_addr must be the same in every lane), written out so that the
+// compiler does not see an LDS write in
+// flight: it would put a full vmcnt(0) in front of every later LDS read,
+// which makes the next chunk's loads finish before the current chunk is
+// multiplied.  The kernel's own vmcnt wait and barrier order the data.
+__device__ __forceinline__ void dma16_to_lds(const void *gptr, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory", "m0");
+}
+
 // Logits phase layout: 256 threads = TG token groups x EG expert groups
 // (EG = 16, or 8 when E <= 8 so that no thread repeats an expert); a thread
 // owns TT tokens (tg + TG i: consecutive lanes read rows 36 floats apart, so
@@ -222,9 +235,8 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
         for (int q = wave; q < n_wdma; q += RT_THREADS / 64) {
             const int blk = q / NSEG, seg = q % NSEG;
             const int r = min(blk * 8 + drow, E - 1);  // rows past E: a copy, never read
-            __builtin_amdgcn_global_load_lds(
-                (gbl_void_t *)(wr + (int64_t)r * H + h0 + seg * 32 + dchunk * 4),
-                (lds_void_t *)(wsb + blk * 8 * HC + seg * 256), 16, 0, 0);
+            dma16_to_lds(wr + (int64_t)r * H + h0 + seg * 32 + dchunk * 4,
+                         (uint32_t)(uintptr_t)(lds_void_t *)(wsb + blk * 8 * HC + seg * 256));
         }
     };
 

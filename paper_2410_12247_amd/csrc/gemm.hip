@@ -584,13 +584,18 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
         const __amdgpu_buffer_rsrc_t pres =
             __builtin_amdgcn_make_buffer_rsrc(a.part, 0, -1, kBufferFlags);
         const int loff = lane * 16;
+        // fragment rows wholly past the valid edge are never stored, so
+        // their partial sums are neither written nor read back (decode-sized
+        // tiles hold one or two valid rows of 320)
 #pragma unroll
-        for (int t = 0; t < C::TN; ++t)
+        for (int m = 0; m < C::TM; ++m) {
+            if (wm * C::WTM + m * 16 >= a.m_valid) break;
 #pragma unroll
-            for (int m = 0; m < C::TM; ++m)
+            for (int t = 0; t < C::TN; ++t)
                 __builtin_amdgcn_raw_buffer_store_b128(
                     __builtin_bit_cast(u32x4, acc[t][m]), pres, loff,
                     a.piece * C::PART_BYTES + wave * C::WAVE_BYTES + (t * C::TM + m) * 1024, 0);
+        }
         return;
     }
 
@@ -792,6 +797,8 @@ __device__ __forceinline__ void fixup_rows(__amdgpu_buffer_rsrc_t pres, int loff
     constexpr int NP = C::TN / 2;
 #pragma unroll 1
     for (int m = 0; m < C::TM; ++m) {
+        // fragment rows wholly past the valid edge: no partials were stored
+        if ((wave >> 1) * C::WTM + m * 16 >= m_valid) break;
         floatx4 sum[2];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {

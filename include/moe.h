@@ -239,7 +239,11 @@ moe_status moe_combine(const moe_dims *dims, int32_t e_first, int32_t e_count,
  * Ordered after prior work on `stream` and finished on `stream`.  When the
  * policy needs row counts on the host (gemm_mode != GROUP or PN > 1) the
  * call blocks the host once on a 4*EL-byte device-to-host copy (AUTO needs
- * the counts only when its threshold can be reached by some expert). */
+ * the counts only when its threshold can be reached by some expert).
+ * Thread safety: calls from several host threads on one device are
+ * serialised inside the library (the side streams, ordering events and the
+ * pinned copy of the counts are per device); moe_last_timing reads the
+ * calling thread's own last timed call. */
 moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe_bf16 *x,
                            const float *w_router, const float *bias,
                            const moe_bf16 *w_gate, const moe_bf16 *w_up,

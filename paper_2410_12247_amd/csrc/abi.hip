@@ -60,8 +60,14 @@ moe_status check_dims(const moe_dims *d) {
     return MOE_OK;
 }
 
-WsLayout ws_layout(const moe_dims *d, bool forward, int nbuckets) {
+bool gather_foldable(const moe_dims &d) {
+    return (uint64_t)d.tokens * (uint64_t)d.hidden * 2u < (uint64_t(1) << 32);
+}
+
+WsLayout ws_layout(const moe_dims *d, const moe_opts *opt) {
     WsLayout L{};
+    const bool forward = opt != nullptr;
+    const int nbuckets = forward ? forward_buckets(d, opt) : d->local_count;
     const int64_t T = d->tokens, k = d->top_k, EL = d->local_count;
     const int64_t nslots = T * k;
     const int64_t NB = nbuckets;
@@ -86,12 +92,16 @@ WsLayout ws_layout(const moe_dims *d, bool forward, int nbuckets) {
         L.offsets = take(sizeof(int32_t) * (NB + 1));
         L.sorted_slot = take(sizeof(int32_t) * L.rcap);
         L.slot_row = take(sizeof(int32_t) * nslots);
-        L.x_perm = take(sizeof(bf16_t) * L.rcap * d->hidden);
+        // gathered token rows: only dense stages (and inputs too large for
+        // the gate/up GEMM's folded gather) read them
+        const bool xperm = opt->gemm_mode != MOE_GEMM_GROUP || !gather_foldable(*d);
+        L.x_perm = take(xperm ? sizeof(bf16_t) * L.rcap * d->hidden : 0);
         L.act = take(sizeof(bf16_t) * L.rcap * d->inter);
         L.y_perm = take(sizeof(float) * L.rcap * d->hidden);
         L.shared_act = take(sizeof(bf16_t) * T * d->shared_inter);
         L.shared_off = take(sizeof(int32_t) * 2);
-        L.split_part = take(gemm_split_bytes());
+        // K-split partials, unless every GEMM is one pass over K
+        L.split_part = take((opt->flags & MOE_FLAG_EXACT_ORDER) ? 0 : gemm_split_bytes());
         L.split_meta = take(sizeof(int32_t) * kSplitMetaInts);
     }
     L.total = o;
@@ -136,9 +146,8 @@ const char *moe_last_error(void) { return g_last_error; }
 
 size_t moe_workspace_bytes(const moe_dims *dims, const moe_opts *opts) {
     if (check_dims(dims) != MOE_OK) return 0;
-    if (!opts) return ws_layout(dims, false, dims->local_count).total;
-    const int nb = forward_buckets(dims, opts);
-    return nb > 0 ? ws_layout(dims, true, nb).total : 0;
+    if (opts && forward_buckets(dims, opts) <= 0) return 0;
+    return ws_layout(dims, opts).total;
 }
 
 moe_status moe_route(const moe_dims *dims, const moe_bf16 *x, const float *w_router,
@@ -161,7 +170,7 @@ moe_status moe_permute(const moe_dims *dims, const int32_t *topk_ids, const moe_
     if (!topk_ids || !counts || !offsets || !sorted_slot || !slot_row)
         return fail(MOE_ERR_INVALID, "moe_permute: NULL index tensor");
     if (x_perm && !x) return fail(MOE_ERR_INVALID, "moe_permute: x_perm given without x");
-    const WsLayout L = ws_layout(dims, false, dims->local_count);
+    const WsLayout L = ws_layout(dims, nullptr);
     if (!ws || ws_bytes < L.total)
         return fail(MOE_ERR_WORKSPACE, "moe_permute: workspace %zu < %zu bytes", ws_bytes,
                     L.total);

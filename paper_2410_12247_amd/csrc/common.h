@@ -59,19 +59,24 @@ struct WsLayout {
     size_t offsets;       // int32 [nbuckets+1]
     size_t sorted_slot;   // int32 [Rcap]
     size_t slot_row;      // int32 [T*k]
-    size_t x_perm;        // bf16  [Rcap][H]
+    size_t x_perm;        // bf16  [Rcap][H] (0 bytes when no stage gathers)
     size_t act;           // bf16  [Rcap][I]
     size_t y_perm;        // fp32  [Rcap][H]
     size_t shared_act;    // bf16  [T][Is]
     size_t shared_off;    // int32 [2] = {0, T}: the shared FFN as one grouped-GEMM expert
-    size_t split_part;    // fp32  grouped-GEMM K-split partials (gemm_split_bytes)
+    size_t split_part;    // fp32  K-split partials (gemm_split_bytes; 0 bytes in exact order)
     size_t split_meta;    // int32 [kSplitMetaInts] K-split tail-tile records
     size_t total;
     int64_t nchunks;
     int64_t rcap;
     int nbuckets;
 };
-WsLayout ws_layout(const moe_dims *d, bool forward, int nbuckets);
+// Layout for moe_permute (o == NULL) or for moe_ffn_forward with options o
+// (valid options: check them first).
+WsLayout ws_layout(const moe_dims *d, const moe_opts *o);
+// The grouped gate/up GEMM can read its token rows straight from x through
+// the dispatch order while every byte offset into x fits 32 bits.
+bool gather_foldable(const moe_dims &d);
 // Dispatch buckets moe_ffn_forward uses with options o (EL, or PN*EL for
 // token-range stages); 0 when the options are not usable.
 int forward_buckets(const moe_dims *d, const moe_opts *o);

@@ -19,6 +19,7 @@
 // expert for large ones).
 #include <algorithm>
 #include <cmath>
+#include <memory>
 #include <mutex>
 #include <vector>
 
@@ -45,16 +46,20 @@ enum Phase {
     PH_ROUTE, PH_PERMUTE, PH_GATHER, PH_GATEUP, PH_DOWN, PH_SHARED, PH_COMBINE, PH_TOTAL, PH_N
 };
 
+// Per-device state of moe_ffn_forward: three side streams and the pinned
+// host copy of the row counts.  `call` is held for a whole call, so two
+// host threads driving the same device take turns (their enqueues do not
+// interleave on the shared streams, events and pinned buffer).
 struct DevState {
+    std::mutex call;
     hipStream_t sg = nullptr, sm = nullptr, sc = nullptr;
     std::vector<hipEvent_t> sync_ev;   // ordering events (no timing)
-    std::vector<hipEvent_t> time_ev;   // timing events
     int32_t *pinned_counts = nullptr;  // host-visible copy of counts
     bool ready = false;
 };
 
-std::mutex g_mu;
-std::vector<DevState> g_dev;
+std::mutex g_mu;  // guards g_dev and the creation of each device's state
+std::vector<std::unique_ptr<DevState>> g_dev;
 
 moe_status ensure_events(std::vector<hipEvent_t> &pool, size_t n, unsigned flags) {
     while (pool.size() < n) {
@@ -70,7 +75,8 @@ moe_status get_state(DevState **out) {
     MOE_HIP(hipGetDevice(&dev));
     std::lock_guard<std::mutex> lock(g_mu);
     if ((int)g_dev.size() <= dev) g_dev.resize(dev + 1);
-    DevState &st = g_dev[dev];
+    if (!g_dev[dev]) g_dev[dev].reset(new DevState);
+    DevState &st = *g_dev[dev];
     if (!st.ready) {
         MOE_HIP(hipStreamCreateWithFlags(&st.sg, hipStreamNonBlocking));
         MOE_HIP(hipStreamCreateWithFlags(&st.sm, hipStreamNonBlocking));
@@ -94,6 +100,9 @@ struct TimingRecord {
     bool valid = false;
 };
 thread_local TimingRecord g_timing;
+// timing events of the calling thread, per device: a thread's last timed
+// call stays readable whatever other threads do
+thread_local std::vector<std::vector<hipEvent_t>> t_time_ev;
 
 // Records spans into the calling thread's record when enabled: every
 // phase (MOE_FLAG_TIMING), or only the GEMM phases (MOE_FLAG_TIMING_GEMM).
@@ -101,8 +110,8 @@ thread_local TimingRecord g_timing;
 // nothing enqueued in between, reuses that span's stop event as its start.
 class Timer {
    public:
-    Timer(DevState *st, int flags)
-        : st_(st), all_((flags & MOE_FLAG_TIMING) != 0),
+    Timer(std::vector<hipEvent_t> *pool, int flags)
+        : pool_(pool), all_((flags & MOE_FLAG_TIMING) != 0),
           gemm_((flags & (MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM)) != 0) {}
     // Starts a span of `phase` on stream s; returns its index (or -1).
     moe_status begin(hipStream_t s, int phase, int *idx = nullptr) {
@@ -116,12 +125,9 @@ class Timer {
         // (the caller's stream may be the null stream: compare only after a
         // span has ended)
         const bool chain = chain_ && last_s_ == s;
-        {
-            std::lock_guard<std::mutex> lock(g_mu);
-            MOE_TRY(ensure_events(st_->time_ev, used_ + 2, hipEventDefault));
-            a = chain ? last_stop_ : st_->time_ev[used_];
-            b = st_->time_ev[used_ + 1];
-        }
+        MOE_TRY(ensure_events(*pool_, used_ + 2, hipEventDefault));
+        a = chain ? last_stop_ : (*pool_)[used_];
+        b = (*pool_)[used_ + 1];
         used_ += 2;
         if (!chain) MOE_HIP(hipEventRecord(a, s));
         chain_ = false;
@@ -145,7 +151,7 @@ class Timer {
     bool timed(int phase) const {
         return all_ || (gemm_ && (phase == PH_GATEUP || phase == PH_DOWN || phase == PH_SHARED));
     }
-    DevState *st_;
+    std::vector<hipEvent_t> *pool_;
     bool all_, gemm_;
     size_t used_ = 0;
     int cur_ = -1;
@@ -184,72 +190,41 @@ int forward_buckets(const moe_dims *d, const moe_opts *o) {
     return o->chunk_mode == MOE_CHUNK_TOKENS ? o->pipeline_n * d->local_count : d->local_count;
 }
 
-}  // namespace moe
+bool needs_host_counts(const moe_dims &d, const moe_opts &o) {
+    const int32_t m_star = o.dense_min_rows > 0 ? o.dense_min_rows : kDefaultDenseMinRows;
+    // row counts are needed on the host to size per-expert dense launches and
+    // stage gathers; AUTO is GROUP without a sync when no expert can reach the
+    // threshold (an expert has at most T rows) and PN = 1
+    return o.gemm_mode == MOE_GEMM_DENSE || o.pipeline_n > 1 ||
+           (o.gemm_mode == MOE_GEMM_AUTO && m_star <= d.tokens);
+}
 
-using namespace moe;
-
-extern "C" {
-
-int32_t moe_default_dense_min_rows(void) { return kDefaultDenseMinRows; }
-
-// The pipeline-number model of the paper's ablation (Sec. 5.2): the overlap
-// hides C/PN of each of PN - 1 stages, and cutting the work costs
-// k*PN + b, so G(PN) = C - b - (C/PN + k*PN) for PN > 1 and G(1) = 0.  The
-// candidates are the divisors of local_count (each stage an equal expert
-// group), searched exhaustively: the closed-form optimum sqrt(C/k) need not
-// be one of them.
-moe_status moe_choose_pipeline_n(double c_ms, double k_ms, double b_ms, int32_t local_count,
-                                 int32_t *pn, double *gain_ms) {
-    if (!pn) return fail(MOE_ERR_INVALID, "moe_choose_pipeline_n: NULL pn");
-    if (!std::isfinite(c_ms) || !std::isfinite(k_ms) || !std::isfinite(b_ms) || c_ms < 0 ||
-        k_ms < 0)
-        return fail(MOE_ERR_INVALID, "moe_choose_pipeline_n: C and k must be finite and >= 0, "
-                                     "b finite");
-    if (local_count < 1 || local_count > kMaxExperts)
-        return fail(MOE_ERR_INVALID, "moe_choose_pipeline_n: local_count %d out of range",
-                    local_count);
-    int32_t best = 1;
-    double best_gain = 0.0;
-    for (int32_t n = 2; n <= local_count; ++n) {
-        if (local_count % n) continue;
-        const double g = c_ms - b_ms - (c_ms / n + k_ms * n);
-        if (g > best_gain) {
-            best = n;
-            best_gain = g;
-        }
-    }
-    *pn = best;
-    if (gain_ms) *gain_ms = best_gain;
+moe_status check_tensors(const moe_dims &d, const moe_bf16 *x, const float *w_router,
+                         const moe_bf16 *w_gate, const moe_bf16 *w_up, const moe_bf16 *w_down,
+                         const moe_bf16 *shared_gate, const moe_bf16 *shared_up,
+                         const moe_bf16 *shared_down, const float *y) {
+    if (!x || !w_router || !w_gate || !w_up || !w_down || !y)
+        return fail(MOE_ERR_INVALID, "moe_ffn_forward: NULL tensor");
+    if (d.shared_inter > 0 && (!shared_gate || !shared_up || !shared_down))
+        return fail(MOE_ERR_INVALID, "moe_ffn_forward: shared_inter > 0 needs shared weights");
     return MOE_OK;
 }
 
-moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe_bf16 *x,
-                           const float *w_router, const float *bias,
-                           const moe_bf16 *w_gate, const moe_bf16 *w_up,
-                           const moe_bf16 *w_down, const moe_bf16 *shared_gate,
-                           const moe_bf16 *shared_up, const moe_bf16 *shared_down,
-                           float *y, int32_t *topk_ids, float *topk_w, int32_t *counts,
-                           void *ws, size_t ws_bytes, void *stream) {
-    MOE_TRY(check_dims(dims));
-    moe_opts defaults{};
-    defaults.pipeline_n = 1;
-    const moe_opts *o = opts ? opts : &defaults;
-    MOE_TRY(check_opts(dims, o));
-    const moe_dims &d = *dims;
-    if (d.tokens == 0) return MOE_OK;
-    if (!x || !w_router || !w_gate || !w_up || !w_down || !y)
-        return fail(MOE_ERR_INVALID, "moe_ffn_forward: NULL tensor");
+// The forward itself, after argument checks: workspace at `base` laid out
+// as L.  st == NULL runs every step on the caller's stream and never needs
+// the row counts on the host.
+moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *x,
+                        const float *w_router, const float *bias, const moe_bf16 *w_gate,
+                        const moe_bf16 *w_up, const moe_bf16 *w_down,
+                        const moe_bf16 *shared_gate, const moe_bf16 *shared_up,
+                        const moe_bf16 *shared_down, float *y, int32_t *topk_ids, float *topk_w,
+                        int32_t *counts, char *base, const WsLayout &L, DevState *st,
+                        hipStream_t s0) {
+    const moe_opts *o = &opt;
     const bool has_shared = d.shared_inter > 0;
-    if (has_shared && (!shared_gate || !shared_up || !shared_down))
-        return fail(MOE_ERR_INVALID, "moe_ffn_forward: shared_inter > 0 needs shared weights");
     const bool tok_stages = o->chunk_mode == MOE_CHUNK_TOKENS;
-    const int NB = forward_buckets(dims, o);
-    const WsLayout L = ws_layout(dims, true, NB);
-    if (!ws || ws_bytes < L.total)
-        return fail(MOE_ERR_WORKSPACE, "moe_ffn_forward: workspace %zu < %zu bytes", ws_bytes,
-                    L.total);
+    const int NB = L.nbuckets;
 
-    char *base = static_cast<char *>(ws);
     int32_t *ids = topk_ids ? topk_ids : reinterpret_cast<int32_t *>(base + L.ids);
     float *wts = topk_w ? topk_w : reinterpret_cast<float *>(base + L.weights);
     // rows per bucket (local expert, or stage * EL + local expert) and their
@@ -266,30 +241,40 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     float *y_perm = reinterpret_cast<float *>(base + L.y_perm);
     bf16_t *shared_act = reinterpret_cast<bf16_t *>(base + L.shared_act);
 
-    DevState *st = nullptr;
-    MOE_TRY(get_state(&st));
     const int PN = o->pipeline_n;
     const int EL = d.local_count;
     const int per_stage = tok_stages ? EL : EL / PN;  // buckets per stage
     const int64_t tps = tok_stages ? (d.tokens + PN - 1) / PN : 0;
-    {
-        std::lock_guard<std::mutex> lock(g_mu);
-        MOE_TRY(ensure_events(st->sync_ev, 3 * (size_t)PN + 4, hipEventDisableTiming));
-    }
-    hipEvent_t ev_fork = st->sync_ev[0], ev_counts = st->sync_ev[1], ev_done = st->sync_ev[2],
-               ev_start = st->sync_ev[3];
-    hipEvent_t *ev_g = &st->sync_ev[4], *ev_m = ev_g + PN;
-
-    const bool timing = (o->flags & (MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM)) != 0;
-    if (timing) g_timing = TimingRecord{};
-    Timer tm(st, o->flags);
-    hipStream_t s0 = (hipStream_t)stream;
     // One stage without shared experts has nothing to overlap: every step
     // runs on the caller's stream (no cross-stream event hops, which cost
     // tens of microseconds each).  So does the serial mode, where nothing
-    // may overlap.  Otherwise gather, GEMMs and combine run on their own
-    // streams so that stages (and the shared FFN) overlap.
-    const bool one_stream = (PN == 1 && !has_shared) || (o->flags & MOE_FLAG_SERIAL) != 0;
+    // may overlap, and a call without device state (no internal streams).
+    // Otherwise gather, GEMMs and combine run on their own streams so that
+    // stages (and the shared FFN) overlap.
+    const bool one_stream =
+        st == nullptr || (PN == 1 && !has_shared) || (o->flags & MOE_FLAG_SERIAL) != 0;
+    hipEvent_t ev_fork = nullptr, ev_counts = nullptr, ev_done = nullptr, ev_start = nullptr;
+    hipEvent_t *ev_g = nullptr, *ev_m = nullptr;
+    if (st) {
+        MOE_TRY(ensure_events(st->sync_ev, 3 * (size_t)PN + 4, hipEventDisableTiming));
+        ev_fork = st->sync_ev[0];
+        ev_counts = st->sync_ev[1];
+        ev_done = st->sync_ev[2];
+        ev_start = st->sync_ev[3];
+        ev_g = &st->sync_ev[4];
+        ev_m = ev_g + PN;
+    }
+
+    const bool timing = st && (o->flags & (MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM)) != 0;
+    std::vector<hipEvent_t> *tpool = nullptr;
+    if (timing) {
+        g_timing = TimingRecord{};
+        int dev = 0;
+        MOE_HIP(hipGetDevice(&dev));
+        if ((int)t_time_ev.size() <= dev) t_time_ev.resize(dev + 1);
+        tpool = &t_time_ev[dev];
+    }
+    Timer tm(tpool, timing ? o->flags : 0);
     hipStream_t sg = one_stream ? s0 : st->sg;
     hipStream_t sm = one_stream ? s0 : st->sm;
     hipStream_t sc = one_stream ? s0 : st->sc;
@@ -337,7 +322,7 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     MOE_HIP(launch_route(d, x, w_router, bias, ids, wts, logits, s0));
     MOE_TRY(tm.end(s0));
     MOE_TRY(tm.begin(s0, PH_PERMUTE));
-    MOE_HIP(launch_permute(d, ids, ws, L, tps, cnt, off, cnt_el, sorted_slot, slot_row, s0));
+    MOE_HIP(launch_permute(d, ids, base, L, tps, cnt, off, cnt_el, sorted_slot, slot_row, s0));
     MOE_TRY(tm.end(s0));
 
     // GEMM kind per stage needs the row counts on the host
@@ -346,10 +331,9 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     // row counts are needed on the host to size per-expert dense launches and
     // stage gathers; AUTO is GROUP without a sync when no expert can reach the
     // threshold (an expert has at most T rows) and PN = 1
-    const bool need_counts =
-        o->gemm_mode == MOE_GEMM_DENSE || PN > 1 ||
-        (o->gemm_mode == MOE_GEMM_AUTO && m_star <= d.tokens);
+    const bool need_counts = needs_host_counts(d, *o);
     if (need_counts) {
+        if (!st) return fail(MOE_ERR_UNSUPPORTED, "row counts needed on the host");
         MOE_HIP(hipMemcpyAsync(st->pinned_counts, cnt, sizeof(int32_t) * NB,
                                hipMemcpyDeviceToHost, s0));
         MOE_HIP(hipEventRecord(ev_counts, s0));
@@ -359,7 +343,7 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     }
     // the grouped gate/up GEMM can gather its token rows itself while every
     // byte offset into x fits 32 bits
-    const bool fold_ok = (uint64_t)T * (uint64_t)H * 2u < (uint64_t(1) << 32);
+    const bool fold_ok = gather_foldable(d);
 
     if (!one_stream) {
         MOE_HIP(hipEventRecord(ev_fork, s0));
@@ -468,6 +452,72 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     MOE_TRY(tm.end(s0, total_span));
     if (timing) g_timing.valid = true;
     return MOE_OK;
+}
+
+}  // namespace moe
+
+using namespace moe;
+
+extern "C" {
+
+int32_t moe_default_dense_min_rows(void) { return kDefaultDenseMinRows; }
+
+// The pipeline-number model of the paper's ablation (Sec. 5.2): the overlap
+// hides C/PN of each of PN - 1 stages, and cutting the work costs
+// k*PN + b, so G(PN) = C - b - (C/PN + k*PN) for PN > 1 and G(1) = 0.  The
+// candidates are the divisors of local_count (each stage an equal expert
+// group), searched exhaustively: the closed-form optimum sqrt(C/k) need not
+// be one of them.
+moe_status moe_choose_pipeline_n(double c_ms, double k_ms, double b_ms, int32_t local_count,
+                                 int32_t *pn, double *gain_ms) {
+    if (!pn) return fail(MOE_ERR_INVALID, "moe_choose_pipeline_n: NULL pn");
+    if (!std::isfinite(c_ms) || !std::isfinite(k_ms) || !std::isfinite(b_ms) || c_ms < 0 ||
+        k_ms < 0)
+        return fail(MOE_ERR_INVALID, "moe_choose_pipeline_n: C and k must be finite and >= 0, "
+                                     "b finite");
+    if (local_count < 1 || local_count > kMaxExperts)
+        return fail(MOE_ERR_INVALID, "moe_choose_pipeline_n: local_count %d out of range",
+                    local_count);
+    int32_t best = 1;
+    double best_gain = 0.0;
+    for (int32_t n = 2; n <= local_count; ++n) {
+        if (local_count % n) continue;
+        const double g = c_ms - b_ms - (c_ms / n + k_ms * n);
+        if (g > best_gain) {
+            best = n;
+            best_gain = g;
+        }
+    }
+    *pn = best;
+    if (gain_ms) *gain_ms = best_gain;
+    return MOE_OK;
+}
+
+moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe_bf16 *x,
+                           const float *w_router, const float *bias,
+                           const moe_bf16 *w_gate, const moe_bf16 *w_up,
+                           const moe_bf16 *w_down, const moe_bf16 *shared_gate,
+                           const moe_bf16 *shared_up, const moe_bf16 *shared_down,
+                           float *y, int32_t *topk_ids, float *topk_w, int32_t *counts,
+                           void *ws, size_t ws_bytes, void *stream) {
+    MOE_TRY(check_dims(dims));
+    moe_opts defaults{};
+    defaults.pipeline_n = 1;
+    const moe_opts *o = opts ? opts : &defaults;
+    MOE_TRY(check_opts(dims, o));
+    if (dims->tokens == 0) return MOE_OK;
+    MOE_TRY(check_tensors(*dims, x, w_router, w_gate, w_up, w_down, shared_gate, shared_up,
+                          shared_down, y));
+    const WsLayout L = ws_layout(dims, o);
+    if (!ws || ws_bytes < L.total)
+        return fail(MOE_ERR_WORKSPACE, "moe_ffn_forward: workspace %zu < %zu bytes", ws_bytes,
+                    L.total);
+    DevState *st = nullptr;
+    MOE_TRY(get_state(&st));
+    std::lock_guard<std::mutex> call(st->call);
+    return forward_impl(*dims, *o, x, w_router, bias, w_gate, w_up, w_down, shared_gate,
+                        shared_up, shared_down, y, topk_ids, topk_w, counts,
+                        static_cast<char *>(ws), L, st, (hipStream_t)stream);
 }
 
 moe_status moe_last_timing(moe_timing *out) {

@@ -155,10 +155,13 @@ __device__ __forceinline__ void select_token(const float *zrow, int64_t t, int E
 // which makes the next chunk's loads finish before the current chunk is
 // multiplied.  The kernel's own vmcnt wait and barrier order the data.
 __device__ __forceinline__ void dma16_to_lds(const void *gptr, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+    // the LDS address goes in through an "{m0}" operand, so the compiler
+    // itself writes m0 (and knows it does); the s_nop separates that write
+    // from the load that reads it
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                  :
-                 : "v"(gptr), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
-                 : "memory", "m0");
+                 : "v"(gptr), "{m0}"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory");
 }
 
 // Logits phase layout: 256 threads = TG token groups x EG expert groups

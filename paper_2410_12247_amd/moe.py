@@ -87,7 +87,8 @@ def lib():
     L.moe_status_string.restype = ctypes.c_char_p
     L.moe_last_error.restype = ctypes.c_char_p
     for name in ("moe_route", "moe_permute", "moe_gather", "moe_ffn_group", "moe_ffn_dense",
-                 "moe_combine", "moe_ffn_forward", "moe_last_timing", "moe_choose_pipeline_n"):
+                 "moe_combine", "moe_ffn_forward", "moe_last_timing",
+                 "moe_choose_pipeline_n"):
         getattr(L, name).restype = I32
     _lib = L
     return L

@@ -184,3 +184,17 @@ def test_pipeline_n_chooser_model():
         with pytest.raises(moe.MoEError) as e:
             ch(*args)
         assert e.value.status == 1
+
+
+def test_workspace_holds_only_what_the_options_use():
+    """Gathered rows only when a stage may run DenseGemm (or the gather cannot
+    be folded into the GEMM), K-split partials only when the grouped GEMM may
+    cut tiles."""
+    d = moe.dims(16384, 4096, 3584, 8, 2)
+    R = 16384 * 2
+    auto = moe.workspace_bytes(d, moe.opts())
+    group = moe.workspace_bytes(d, moe.opts(gemm_mode=moe.GEMM_GROUP))
+    exact = moe.workspace_bytes(d, moe.opts(gemm_mode=moe.GEMM_GROUP, exact_order=True))
+    assert auto - group >= R * 4096 * 2                      # x_perm [R][H] bf16
+    assert group - exact >= 256 * 256 * 320 * 4              # 256 partial tiles of fp32
+    assert exact >= R * (3584 * 2 + 4096 * 4)                # act + y_perm

@@ -32,6 +32,11 @@ CASES = {
     # few experts with many rows each: several grouped token tiles per expert
     # plus a ragged last one
     "tall4": C(name="tall4", index=209, T=1500, H=192, I=320, E=4, EL=4, k=2, renorm=True),
+    # many buckets and chunks: 160 local experts of 256 (the dispatch scan
+    # over more than one wave of buckets), top-8, 24000 slots (24 histogram
+    # chunks: the scan's sixteen-chunk unrolled loop plus a remainder)
+    "wide": C(name="wide", index=218, T=3000, H=128, I=64, E=256, EL=160, e0=50, k=8,
+              renorm=True),
 }
 # Shapes whose grouped GEMMs leave a partial last round on a 256-workgroup
 # grid with K long enough to be cut (pieces of at least 32 K stages of 32):

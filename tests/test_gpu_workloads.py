@@ -1,8 +1,9 @@
 """GPU parity at the full workload sizes, in the launch configuration the
-benchmark times (moe_ffn_forward).  Routing, counts and the permutation are
-compared element by element with the oracle on every token; the FFN output
-on a sample of tokens the oracle computes one by one (full-size oracle FFNs
-take minutes on the host)."""
+benchmark times (moe_ffn_forward).  Routing ids and weights, counts, offsets
+and the whole permutation (sorted_slot, slot_row) are compared element by
+element with the oracle on every token; the FFN output on a sample of tokens
+the oracle computes one by one (full-size oracle FFNs take minutes on the
+host)."""
 import numpy as np
 import pytest
 import torch
@@ -15,7 +16,8 @@ from gpu_util import Dev, assert_close
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 WORKLOADS = [("tiny", None), ("mixtral", None), ("dbrx", None), ("dsv2", None),
-             ("zipf", 64), ("zipf", 4096), ("zipf", 65536),
+             ("zipf", 64), ("zipf", 256), ("zipf", 1024), ("zipf", 4096), ("zipf", 16384),
+             ("zipf", 65536),
              # expert-parallel shares as the paper deploys them, and decode
              ("mixtral_ep", None), ("dbrx_ep", None), ("mixtral", 1), ("mixtral", 64)]
 SAMPLE = 24  # tokens per workload checked against the oracle FFN
@@ -56,6 +58,21 @@ def test_full_workload(name, T):
     assert np.all(np.abs(w_g.astype(np.float64) - w) <= 2.0 ** -23 * np.abs(w) + 1e-30)
     counts, offsets, sorted_slot, slot_row = oracle.dispatch(ids, shp.e0, shp.EL)
     assert np.array_equal(buf.counts.cpu().numpy(), counts)
+    # the dispatch of the same ids through moe_permute (the kernels the
+    # forward runs, at this size: every chunk of the histogram and scan)
+    R = int(offsets[-1])
+    gc = torch.empty(shp.EL, dtype=torch.int32, device=y.device)
+    go = torch.empty(shp.EL + 1, dtype=torch.int32, device=y.device)
+    gss = torch.full((shp.T * min(shp.k, shp.EL),), -7, dtype=torch.int32, device=y.device)
+    gsr = torch.empty(shp.T * shp.k, dtype=torch.int32, device=y.device)
+    ws = torch.empty(moe.workspace_bytes(g.d), dtype=torch.uint8, device=y.device)
+    moe.permute(g.d, buf.topk_ids, None, gc, go, gss, gsr, None, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(gc.cpu().numpy(), counts)
+    assert np.array_equal(go.cpu().numpy(), offsets)
+    assert np.array_equal(gss.cpu().numpy()[:R], sorted_slot)
+    assert np.array_equal(gsr.cpu().numpy(), slot_row)
+    del gc, go, gss, gsr, ws
 
     # FFN output on sampled tokens
     loc = (ids >= shp.e0) & (ids < shp.e0 + shp.EL)

@@ -312,3 +312,69 @@ def test_zipf_bias_skews_popularity():
     rank = per * (np.arange(160) % 20) + np.arange(160) // 20 + 1
     top = cnt[np.argsort(rank)]
     assert top[:8].sum() > 10 * max(1, top[-80:].sum() // 10)
+
+
+# ----------------------------------------------- row list and combine init ---
+
+def test_expert_row_list_matches_library_swiglu_per_pair():
+    """oracle.expert_row_list on an arbitrary list of (token, local expert)
+    pairs (repeats, every expert, tokens out of order) against the SwiGLU of
+    that token through that expert with torch fp64 library ops, rounded to
+    fp32 once.  A wrong token index, a wrong expert stack or a transposed
+    down matrix changes whole rows."""
+    E, T, H, I = 5, 17, 64, 96
+    inp = _small_case(T=T, H=H, I=I, E=E, EL=E, k=2, renorm=True, seed=17)
+    rng = np.random.default_rng(17)
+    tok = np.concatenate([rng.integers(0, T, size=30), [T - 1, 0, 0]]).astype(np.int64)
+    el = np.concatenate([rng.integers(0, E, size=30), [E - 1, 0, E - 1]]).astype(np.int32)
+    y = oracle.expert_row_list(inp.x, tok, el, inp.w_gate, inp.w_up, inp.w_down)
+    x = _f64(inp.x)
+    for n in range(len(tok)):
+        e = int(el[n])
+        ref = _swiglu_torch(x[tok[n]:tok[n] + 1], _f64(inp.w_gate[e]), _f64(inp.w_up[e]),
+                            _f64(inp.w_down[e]))[0]
+        assert np.allclose(y[n], ref, rtol=1e-6, atol=1e-7), (n, int(tok[n]), e)
+    # the list path and the dispatched-row path give the same bits for the
+    # same (token, expert) rows
+    _, ids, _ = oracle.route(inp.x, inp.w_router, None, 2, True)
+    counts, offsets, sorted_slot, _ = oracle.dispatch(ids, 0, E)
+    yp = oracle.expert_rows(inp.x, sorted_slot, offsets, inp.w_gate, inp.w_up, inp.w_down, 2)
+    yl = oracle.expert_row_list(inp.x, sorted_slot // 2, np.repeat(np.arange(E), counts),
+                                inp.w_gate, inp.w_up, inp.w_down)
+    assert np.array_equal(yl, yp)
+
+
+def test_combine_with_initial_value_is_a_sparse_matrix_product():
+    """oracle.combine(y_perm, slot_row, w, y_init): y = y_init + A y_perm,
+    where A [T, R] holds w[t, j] at column slot_row[t, j] (no entry for a
+    non-local slot), computed here as one torch fp64 matrix product.  Also
+    the special cases that leave y_init untouched (zero weights, zero rows)."""
+    E, EL, e0, k, T, H = 8, 5, 2, 3, 40, 24
+    rng = np.random.default_rng(18)
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    counts, offsets, sorted_slot, slot_row = oracle.dispatch(ids, e0, EL)
+    R = int(offsets[-1])
+    assert 0 < R < T * k  # some slots are not local
+    y_perm = rng.standard_normal((R, H)).astype(np.float32)
+    w = rng.random((T, k)).astype(np.float32)
+    y_init = rng.standard_normal((T, H)).astype(np.float32)
+    sr = slot_row.reshape(T, k)
+    y = oracle.combine(y_perm, sr, w, y_init)
+    A = np.zeros((T, R))
+    for t in range(T):
+        for j in range(k):
+            if sr[t, j] >= 0:
+                A[t, sr[t, j]] += float(w[t, j])
+    ref = (torch.from_numpy(y_init.astype(np.float64)) +
+           torch.from_numpy(A) @ torch.from_numpy(y_perm.astype(np.float64))).numpy()
+    assert np.allclose(y, ref, rtol=2.0 ** -23, atol=1e-30)
+    # with an initial value the result differs from the plain combine by it
+    y0 = oracle.combine(y_perm, sr, w)
+    assert np.allclose(y.astype(np.float64) - y0, y_init, rtol=1e-6, atol=1e-6)
+    # nothing to add: y_init comes back bit for bit
+    assert np.array_equal(oracle.combine(y_perm, sr, np.zeros_like(w), y_init), y_init)
+    assert np.array_equal(oracle.combine(np.zeros_like(y_perm), sr, w, y_init), y_init)
+    # no local slot at all: y_init again, and zeros without it
+    none = np.full_like(sr, -1)
+    assert np.array_equal(oracle.combine(y_perm, none, w, y_init), y_init)
+    assert np.all(oracle.combine(y_perm, none, w) == 0.0)

@@ -252,6 +252,31 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
                            float *y, int32_t *topk_ids, float *topk_w, int32_t *counts,
                            void *ws, size_t ws_bytes, void *stream);
 
+/* moe_ffn_forward for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation, arguments and bits as moe_ffn_forward with the same
+ * options, but it takes no workspace.  Its scratch is a static device buffer
+ * of 256 MiB in the library (each device the library runs on holds its own
+ * copy until the process ends); the call allocates nothing, on the device or
+ * the host.  Limits: moe_workspace_bytes(dims, opts) must not exceed
+ * 256 MiB (e.g. up to 512 tokens of the Mixtral-, DBRX- and DeepSeekV2-shaped
+ * layers, or decode batches), else MOE_ERR_UNSUPPORTED; options that need
+ * the row counts on the host (pipeline_n > 1, MOE_GEMM_DENSE, or an AUTO
+ * threshold some expert can reach) and the timing flags are refused with
+ * MOE_ERR_UNSUPPORTED; every step runs on `stream` (shared experts
+ * included), with the same bits as with side streams.  All calls on one
+ * device share the buffer, and it keeps the last call's contents: calls from
+ * several host threads are serialised, but calls that overlap on the GPU
+ * (this one still running when another is enqueued on another stream) race
+ * on it.  Nothing in the buffer needs to start zeroed. */
+moe_status moe_ffn_forward_noalloc(const moe_dims *dims, const moe_opts *opts,
+                                   const moe_bf16 *x, const float *w_router, const float *bias,
+                                   const moe_bf16 *w_gate, const moe_bf16 *w_up,
+                                   const moe_bf16 *w_down, const moe_bf16 *shared_gate,
+                                   const moe_bf16 *shared_up, const moe_bf16 *shared_down,
+                                   float *y, int32_t *topk_ids, float *topk_w, int32_t *counts,
+                                   void *stream);
+
 /* Timing of the last timed moe_ffn_forward on this thread (waits for its
  * events).  Returns MOE_ERR_INVALID when no timed call was made. */
 moe_status moe_last_timing(moe_timing *out);

@@ -95,6 +95,9 @@ constexpr int kSplitMetaInts = 2 + 4 * (kSplitSlots / 2);
 // Bytes of the partial-accumulator buffer the grouped GEMM takes (all slots).
 size_t gemm_split_bytes();
 
+// Scratch of moe_ffn_forward_noalloc (a static device array per device).
+constexpr size_t kNoAllocScratchBytes = size_t(256) << 20;
+
 // ---- kernel launchers (stream-ordered, no host synchronisation) ----------
 // logits: [T][E] fp32 scratch (may be NULL) for the many-expert, few-token
 // path (T <= kRouteStreamMaxTokens).

@@ -199,6 +199,30 @@ bool needs_host_counts(const moe_dims &d, const moe_opts &o) {
            (o.gemm_mode == MOE_GEMM_AUTO && m_star <= d.tokens);
 }
 
+// Scratch of the no-allocation entry point: one static buffer per device
+// (each device holds its own copy of the array), reached through the address
+// hipGetSymbolAddress gives for the current device.  Calls on one device
+// share it, so they are serialised by g_noalloc_mu on the host; calls that
+// overlap on the GPU (other streams, other processes do not share it) race.
+__device__ __align__(256) char scratch[kNoAllocScratchBytes];
+std::mutex g_noalloc_mu;
+std::vector<char *> g_scratch_ptr;  // per device, under g_mu
+
+moe_status noalloc_scratch(char **out) {
+    int dev = 0;
+    MOE_HIP(hipGetDevice(&dev));
+    std::lock_guard<std::mutex> lock(g_mu);
+    if ((int)g_scratch_ptr.size() <= dev) g_scratch_ptr.resize(dev + 1, nullptr);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        MOE_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return fail(MOE_ERR_HIP, "hipGetSymbolAddress(scratch) gave NULL");
+        g_scratch_ptr[dev] = static_cast<char *>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return MOE_OK;
+}
+
 moe_status check_tensors(const moe_dims &d, const moe_bf16 *x, const float *w_router,
                          const moe_bf16 *w_gate, const moe_bf16 *w_up, const moe_bf16 *w_down,
                          const moe_bf16 *shared_gate, const moe_bf16 *shared_up,
@@ -211,8 +235,8 @@ moe_status check_tensors(const moe_dims &d, const moe_bf16 *x, const float *w_ro
 }
 
 // The forward itself, after argument checks: workspace at `base` laid out
-// as L.  st == NULL runs every step on the caller's stream and never needs
-// the row counts on the host.
+// as L.  st == NULL (the no-allocation entry point) runs every step on the
+// caller's stream and never needs the row counts on the host.
 moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *x,
                         const float *w_router, const float *bias, const moe_bf16 *w_gate,
                         const moe_bf16 *w_up, const moe_bf16 *w_down,
@@ -248,7 +272,7 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
     // One stage without shared experts has nothing to overlap: every step
     // runs on the caller's stream (no cross-stream event hops, which cost
     // tens of microseconds each).  So does the serial mode, where nothing
-    // may overlap, and a call without device state (no internal streams).
+    // may overlap, and the no-allocation entry point (no internal streams).
     // Otherwise gather, GEMMs and combine run on their own streams so that
     // stages (and the shared FFN) overlap.
     const bool one_stream =
@@ -518,6 +542,41 @@ moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe
     return forward_impl(*dims, *o, x, w_router, bias, w_gate, w_up, w_down, shared_gate,
                         shared_up, shared_down, y, topk_ids, topk_w, counts,
                         static_cast<char *>(ws), L, st, (hipStream_t)stream);
+}
+
+moe_status moe_ffn_forward_noalloc(const moe_dims *dims, const moe_opts *opts,
+                                   const moe_bf16 *x, const float *w_router, const float *bias,
+                                   const moe_bf16 *w_gate, const moe_bf16 *w_up,
+                                   const moe_bf16 *w_down, const moe_bf16 *shared_gate,
+                                   const moe_bf16 *shared_up, const moe_bf16 *shared_down,
+                                   float *y, int32_t *topk_ids, float *topk_w, int32_t *counts,
+                                   void *stream) {
+    MOE_TRY(check_dims(dims));
+    moe_opts defaults{};
+    defaults.pipeline_n = 1;
+    const moe_opts *o = opts ? opts : &defaults;
+    MOE_TRY(check_opts(dims, o));
+    if (o->flags & (MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM))
+        return fail(MOE_ERR_UNSUPPORTED, "moe_ffn_forward_noalloc: no timing flags");
+    if (needs_host_counts(*dims, *o))
+        return fail(MOE_ERR_UNSUPPORTED,
+                    "moe_ffn_forward_noalloc: options need the row counts on the host "
+                    "(pipeline_n > 1, DenseGemm, or an AUTO threshold within reach)");
+    if (dims->tokens == 0) return MOE_OK;
+    MOE_TRY(check_tensors(*dims, x, w_router, w_gate, w_up, w_down, shared_gate, shared_up,
+                          shared_down, y));
+    const WsLayout L = ws_layout(dims, o);
+    if (L.total > kNoAllocScratchBytes)
+        return fail(MOE_ERR_UNSUPPORTED,
+                    "moe_ffn_forward_noalloc: needs %zu bytes of scratch, the built-in "
+                    "buffer holds %zu",
+                    L.total, kNoAllocScratchBytes);
+    char *base = nullptr;
+    MOE_TRY(noalloc_scratch(&base));
+    std::lock_guard<std::mutex> call(g_noalloc_mu);
+    return forward_impl(*dims, *o, x, w_router, bias, w_gate, w_up, w_down, shared_gate,
+                        shared_up, shared_down, y, topk_ids, topk_w, counts, base, L, nullptr,
+                        (hipStream_t)stream);
 }
 
 moe_status moe_last_timing(moe_timing *out) {

@@ -22,7 +22,8 @@ FLAG_TIMING, FLAG_TIMING_GEMM, FLAG_EXACT_ORDER, FLAG_SERIAL = 1, 2, 4, 8
 
 # the entry points include/moe.h declares
 EXPORTS = ("moe_workspace_bytes", "moe_route", "moe_permute", "moe_gather", "moe_ffn_group",
-           "moe_ffn_dense", "moe_combine", "moe_ffn_forward", "moe_last_timing",
+           "moe_ffn_dense", "moe_combine", "moe_ffn_forward", "moe_ffn_forward_noalloc",
+           "moe_last_timing",
            "moe_default_dense_min_rows", "moe_choose_pipeline_n", "moe_status_string",
            "moe_last_error")
 
@@ -79,6 +80,7 @@ def lib():
     L.moe_ffn_dense.argtypes = [I64, I32, I32, P, P, P, P, P, P, P]
     L.moe_combine.argtypes = [D, I32, I32, P, P, P, P, P, I32, P]
     L.moe_ffn_forward.argtypes = [D, O, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    L.moe_ffn_forward_noalloc.argtypes = [D, O, P, P, P, P, P, P, P, P, P, P, P, P, P, P]
     L.moe_last_timing.argtypes = [ctypes.POINTER(Timing)]
     L.moe_default_dense_min_rows.restype = I32
     L.moe_choose_pipeline_n.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double, I32,
@@ -87,7 +89,7 @@ def lib():
     L.moe_status_string.restype = ctypes.c_char_p
     L.moe_last_error.restype = ctypes.c_char_p
     for name in ("moe_route", "moe_permute", "moe_gather", "moe_ffn_group", "moe_ffn_dense",
-                 "moe_combine", "moe_ffn_forward", "moe_last_timing",
+                 "moe_combine", "moe_ffn_forward", "moe_ffn_forward_noalloc", "moe_last_timing",
                  "moe_choose_pipeline_n"):
         getattr(L, name).restype = I32
     _lib = L
@@ -184,6 +186,16 @@ def forward(d, o, x, w_router, bias, w_gate, w_up, w_down, shared_gate, shared_u
                                  _p(w_down), _p(shared_gate), _p(shared_up), _p(shared_down),
                                  _p(y), _p(topk_ids), _p(topk_w), _p(counts), _p(ws),
                                  ws.numel() * ws.element_size(), _s(stream)))
+
+
+def forward_noalloc(d, o, x, w_router, bias, w_gate, w_up, w_down, shared_gate, shared_up,
+                    shared_down, y, topk_ids, topk_w, counts, stream=None):
+    """moe_ffn_forward_noalloc: the forward with the library's static scratch
+    buffer instead of a workspace (no allocation in the call)."""
+    _check(lib().moe_ffn_forward_noalloc(
+        ctypes.byref(d), ctypes.byref(o) if o is not None else None, _p(x), _p(w_router),
+        _p(bias), _p(w_gate), _p(w_up), _p(w_down), _p(shared_gate), _p(shared_up),
+        _p(shared_down), _p(y), _p(topk_ids), _p(topk_w), _p(counts), _s(stream)))
 
 
 def choose_pipeline_n(c_ms: float, k_ms: float, b_ms: float, local_count: int):

@@ -198,3 +198,30 @@ def test_workspace_holds_only_what_the_options_use():
     assert auto - group >= R * 4096 * 2                      # x_perm [R][H] bf16
     assert group - exact >= 256 * 256 * 320 * 4              # 256 partial tiles of fp32
     assert exact >= R * (3584 * 2 + 4096 * 4)                # act + y_perm
+
+
+def test_noalloc_forward_rejects_on_the_host():
+    """moe_ffn_forward_noalloc refuses, before touching the GPU, what it
+    cannot do without allocating: options that need row counts on the host,
+    timing, and workloads whose workspace exceeds its 256 MiB buffer."""
+    L = moe.lib()
+    fake = ctypes.c_void_p(16)  # never dereferenced: validation fails first
+
+    def call(d, o):
+        return L.moe_ffn_forward_noalloc(ctypes.byref(d), ctypes.byref(o) if o else None, fake,
+                                         fake, None, fake, fake, fake, None, None, None, fake,
+                                         None, None, None, None)
+
+    small = moe.dims(64, 256, 128, 8, 2)
+    for o in (moe.opts(pipeline_n=2), moe.opts(gemm_mode=moe.GEMM_DENSE),
+              moe.opts(dense_min_rows=16), moe.opts(timing=True), moe.opts(timing="gemm")):
+        assert call(small, o) == 2, L.moe_last_error()
+    assert call(small, moe.opts(pipeline_n=3)) == 1          # invalid as in moe_ffn_forward
+    big = moe.dims(16384, 4096, 3584, 8, 2)                   # the Mixtral-shaped shard
+    assert moe.workspace_bytes(big, moe.opts()) > 256 << 20
+    assert call(big, moe.opts()) == 2
+    assert b"256" in L.moe_last_error() or b"268435456" in L.moe_last_error()
+    assert L.moe_ffn_forward_noalloc(ctypes.byref(small), None, None, fake, None, fake, fake,
+                                     fake, None, None, None, fake, None, None, None, None) == 1
+    zero = moe.dims(0, 256, 128, 8, 2)
+    assert call(zero, moe.opts()) == 0

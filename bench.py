@@ -74,6 +74,9 @@ def parse_args(argv=None):
     p.add_argument("--gemm-study", action="store_true",
                    help="GroupGemm throughput over group counts, rows per group and CU "
                         "budgets on the DeepSeekV2 expert shape")
+    p.add_argument("--tile-study", action="store_true",
+                   help="DenseGemm launch time of one expert for every tile height and "
+                        "row count (the data of the launch-cost model)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                    help="only run a plain device copy of BYTES (HBM counter calibration)")
     return p.parse_args(argv)
@@ -236,6 +239,8 @@ def main(argv=None):
         return cu_sweep(args)
     if args.gemm_study:
         return gemm_study(args)
+    if args.tile_study:
+        return tile_study(args)
     shape = synth.SHAPES[args.config]
     if args.tokens:
         shape = shape.with_tokens(args.tokens)
@@ -327,29 +332,41 @@ def main(argv=None):
 
 def sweep(args):
     """GroupGemm-forced vs DenseGemm-forced vs AUTO over the zipf token counts
-    on identical routing; one JSON line per point."""
-    from paper_2410_12247_amd import synth
+    on identical routing, with all 20 local experts in one stage (PN = 1) and
+    with one expert per stage (PN = 20, where the paper's Sec. 4.3 has the
+    grouped GEMM become a dense one); one JSON line per point."""
+    from paper_2410_12247_amd import moe, synth
 
     base = synth.SHAPES["zipf"]
     for T in synth.ZIPF_TOKENS:
         shape = base.with_tokens(T)
         inp = synth.make_inputs(shape)
-        res = {}
-        for mode in ("group", "dense", "auto"):
-            a = argparse.Namespace(**{**vars(args), "mode": mode})
-            wall, tms, counts = run_workload(a, shape, inp, args.steps, args.warmup,
-                                             timing="gemm")
-            tm = summarize_timing(tms)
-            res[mode] = {"ms": round(wall / args.steps * 1e3, 4),
-                         "gemm_ms": round(tm["gateup_ms"] + tm["down_ms"], 4),
-                         "dense_stages": tm["dense_stages"]}
-        fg, fd, _ = gemm_flops(shape, int(counts.sum()))
-        best = min(res["group"]["gemm_ms"], res["dense"]["gemm_ms"])
-        print(json.dumps({"sweep": "zipf", "tokens": T, "routed_rows": int(counts.sum()),
-                          "rows_per_expert": counts.tolist(),
-                          "gemm_gflop": round((fg + fd) / 1e9, 2), **res,
-                          "auto_regret": round(res["auto"]["gemm_ms"] / best - 1, 4)}),
-              flush=True)
+        for pn in (1, shape.EL):
+            res = {}
+            for mode in ("group", "dense", "auto"):
+                a = argparse.Namespace(**{**vars(args), "mode": mode, "pn": pn})
+                wall, tms, counts = run_workload(a, shape, inp, args.steps, args.warmup,
+                                                 timing="gemm")
+                tm = summarize_timing(tms)
+                res[mode] = {"ms": round(wall / args.steps * 1e3, 4),
+                             "gemm_ms": round(tm["gateup_ms"] + tm["down_ms"], 4),
+                             "dense_stages": tm["dense_stages"]}
+            fg, fd, _ = gemm_flops(shape, int(counts.sum()))
+            best = min(res["group"]["gemm_ms"], res["dense"]["gemm_ms"])
+            d = moe.dims(shape.T, shape.H, shape.I, shape.E, shape.k, shape.e0, shape.EL,
+                         shape.renorm)
+            per = shape.EL // pn
+            tiles = []
+            for st in range(pn):
+                tiles += moe.gemm_plan(d, moe.opts(gemm_mode=moe.GEMM_DENSE),
+                                       counts[st * per:(st + 1) * per])[1]
+            print(json.dumps({"sweep": "zipf", "tokens": T, "pipeline_n": pn,
+                              "routed_rows": int(counts.sum()),
+                              "rows_per_expert": counts.tolist(),
+                              "dense_tile_rows": tiles,
+                              "gemm_gflop": round((fg + fd) / 1e9, 2), **res,
+                              "auto_regret": round(res["auto"]["gemm_ms"] / best - 1, 4)}),
+                  flush=True)
     return 0
 
 
@@ -472,7 +489,8 @@ def gemm_study(args):
     per group, relative to the best group count of the same rows (Fig. 4b),
     and over the CU budget at 6144 rows per group (Fig. 4c); then GroupGemm
     against one DenseGemm launch per expert at uniform load, 16 experts of m
-    rows each (Fig. 4a).  Inputs are seeded Gaussian bf16 tensors; the rows of
+    rows each (Fig. 4a) and a single expert of m rows (Sec. 4.3's E = N).
+    Inputs are seeded Gaussian bf16 tensors; the rows of
     each group are contiguous."""
     import torch
 
@@ -537,13 +555,60 @@ def gemm_study(args):
         ms = ev[0].elapsed_time(ev[1]) / args.steps
         return ms, 6.0 * G * m * H * I / (ms * 1e-3) / 1e12
 
-    for m in (128, 512, 1024, 2048, 4096, 6144):
-        g_ms, g_tf = time_group(16, m, 0)
-        d_ms, d_tf = time_dense(16, m)
-        print(json.dumps({"gemm_study": "group_vs_dense", "experts": 16, "rows_per_expert": m,
-                          "group_ms": round(g_ms, 4), "dense_ms": round(d_ms, 4),
-                          "group_tflops": round(g_tf, 1), "dense_tflops": round(d_tf, 1)}),
-              flush=True)
+    for G in (16, 1):
+        for m in (128, 512, 1024, 2048, 4096, 6144):
+            g_ms, g_tf = time_group(G, m, 0)
+            d_ms, d_tf = time_dense(G, m)
+            dd = moe.dims(G * m, H, I, G, 1)
+            _, tiles, _, _ = moe.gemm_plan(dd, moe.opts(gemm_mode=moe.GEMM_DENSE,
+                                                        exact_order=True), [m])
+            print(json.dumps({"gemm_study": "group_vs_dense", "experts": G,
+                              "rows_per_expert": m, "group_ms": round(g_ms, 4),
+                              "dense_ms": round(d_ms, 4), "group_tflops": round(g_tf, 1),
+                              "dense_tflops": round(d_tf, 1), "dense_tile_rows": tiles[0]}),
+                  flush=True)
+    return 0
+
+
+def tile_study(args):
+    """One expert's gate/up and down GEMMs as DenseGemm launches with each
+    tile height (128, 192, 256, 320 token rows), over row counts, on the
+    DeepSeekV2 and Mixtral expert shapes; the data the launch-cost model's
+    per-tile step and epilogue costs are fitted to.  Every token is routed
+    to the one expert (E = 1, k = 1), so the launch covers m rows; times are
+    HIP events around each GEMM launch (MOE_FLAG_TIMING_GEMM), in exact order
+    (no K split: a launch is whole rounds of tiles) and with the K split of
+    a partial last round."""
+    from paper_2410_12247_amd import moe, synth
+    from paper_2410_12247_amd.workload import DeviceInputs
+
+    for H, I, label in ((5120, 1536, "dsv2_expert"), (4096, 3584, "mixtral_expert")):
+        for m in (512, 1024, 2048, 4096, 8192, 16384, 32768):
+            shp = synth.custom_shape(name=f"tile{m}", index=230, T=m, H=H, I=I, E=1, EL=1,
+                                     k=1, renorm=True)
+            g = DeviceInputs(synth.make_inputs(shp))
+            for exact in (True, False):
+                res = {}
+                for bm in (128, 192, 256, 320):
+                    o = moe.opts(gemm_mode=moe.GEMM_DENSE, dense_tile_rows=bm, timing="gemm",
+                                 exact_order=exact)
+                    buf = g.buffers(o)
+                    for _ in range(args.warmup):
+                        g.run(buf)
+                    tms = []
+                    for _ in range(args.steps):
+                        g.run(buf)
+                        tms.append(moe.last_timing())
+                    tm = summarize_timing(tms)
+                    res[bm] = {"gateup_us": round(tm["gateup_ms"] * 1e3, 2),
+                               "down_us": round(tm["down_ms"] * 1e3, 2)}
+                    del buf
+                _, tiles, gus, dus = moe.gemm_plan(g.d, moe.opts(exact_order=exact), [m])
+                print(json.dumps({"tile_study": label, "hidden": H, "inter": I, "rows": m,
+                                  "k_split": not exact, "by_tile_rows": res,
+                                  "model_pick": tiles[0], "model_dense_us": round(dus, 1)}),
+                      flush=True)
+            del g
     return 0
 
 

@@ -92,10 +92,14 @@ enum {
  * Both modes give the same bits under MOE_FLAG_EXACT_ORDER. */
 typedef struct {
     int32_t gemm_mode;      /* MOE_GEMM_AUTO, _GROUP or _DENSE */
-    int32_t dense_min_rows; /* AUTO picks DenseGemm for a pipeline stage when
-                               every expert in it has at least this many
-                               rows, else GroupGemm; 0 = built-in default
-                               (see moe_default_dense_min_rows) */
+    int32_t dense_min_rows; /* 0: AUTO weighs GroupGemm against DenseGemm
+                               for each stage of at most two experts with
+                               the library's launch-cost model (see
+                               moe_gemm_plan) and takes GroupGemm for larger
+                               stages.  > 0: AUTO picks DenseGemm for a
+                               stage when every expert in it has at least
+                               this many rows (Sec. 3.2 Conclusion 1's
+                               threshold m), else GroupGemm */
     int32_t pipeline_n;     /* PN >= 1, the number of pipeline stages */
     int32_t gemm_cu_budget; /* workgroups of the persistent grouped GEMM;
                                0 = one per compute unit */
@@ -119,7 +123,11 @@ typedef struct {
                                measures what cutting the work into PN stages
                                costs by itself.  Same bits as without it. */
     int32_t chunk_mode;     /* MOE_CHUNK_EXPERTS or MOE_CHUNK_TOKENS */
-    int32_t reserved[2];    /* must be zero */
+    int32_t dense_tile_rows;/* token rows of a DenseGemm tile: 0 = chosen per
+                               expert from its row count (the height whose
+                               tile count fills the chip best), or 128, 192,
+                               256, 320 to force one */
+    int32_t reserved[1];    /* must be zero */
 } moe_opts;
 
 /* Per-phase device time of the last moe_ffn_forward call on this thread
@@ -199,7 +207,8 @@ moe_status moe_ffn_group(const moe_dims *dims, int32_t e_first, int32_t e_count,
 
 /* DenseGemm expert FFN (Sec. 4.3: with one expert per pipeline stage the
  * grouped GEMM becomes a dense one): one dense SwiGLU FFN over `rows`
- * contiguous rows whose count is known on the host:
+ * contiguous rows whose count is known on the host, so the launch takes the
+ * tile height (128 to 320 token rows) whose tile count fills the chip best:
  *   act[r] = bf16(silu(w_gate x[r]) * (w_up x[r])),  y[r] = w_down act[r]
  * x [rows][hidden] bf16; w_gate, w_up [inter][hidden]; w_down
  * [hidden][inter]; act [rows][inter] bf16 scratch; y [rows][hidden] fp32.
@@ -281,10 +290,23 @@ moe_status moe_ffn_forward_noalloc(const moe_dims *dims, const moe_opts *opts,
  * events).  Returns MOE_ERR_INVALID when no timed call was made. */
 moe_status moe_last_timing(moe_timing *out);
 
-/* The dense-GEMM threshold (rows per expert) AUTO uses when
- * dense_min_rows == 0.  On MI355X the grouped GEMM won at every measured
- * load, so the built-in value (2^30) is never reached. */
-int32_t moe_default_dense_min_rows(void);
+/* The GEMM plan AUTO makes for one pipeline stage (Sec. 3.2 Conclusion 1:
+ * GroupGemm and DenseGemm each win over part of the load range; Sec. 4.3:
+ * with one expert per stage the grouped GEMM becomes a dense one), from the
+ * host row counts of its n_experts experts, rows[0..n_experts).  The model
+ * prices each launch from measured per-tile costs of every tile height:
+ * GroupGemm is one launch over the stage with 320-row tiles; DenseGemm is
+ * one launch per expert with its own tile height.  Writes *dense (1 when
+ * the stage would run DenseGemm under opts->gemm_mode, AUTO included) and,
+ * when not NULL, tile_rows[e] (the tile height of expert e's launch, 0 for
+ * an empty expert), *group_us and *dense_us (predicted GEMM microseconds
+ * of the two kinds).  Uses dims->hidden / inter, opts->gemm_cu_budget,
+ * dense_min_rows, dense_tile_rows and MOE_FLAG_EXACT_ORDER.  Host-only;
+ * never touches the GPU (the grid is the current device's CU count, 256
+ * when no device is visible). */
+moe_status moe_gemm_plan(const moe_dims *dims, const moe_opts *opts, int32_t n_experts,
+                         const int32_t *rows, int32_t *dense, int32_t *tile_rows,
+                         double *group_us, double *dense_us);
 
 /* Pipeline number from the overhead model of the paper's ablation (Sec. 5.2):
  * PN stages hide (PN - 1)/PN of C = min(T_comm, T_comp), the smaller of the

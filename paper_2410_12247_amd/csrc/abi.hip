@@ -92,9 +92,9 @@ WsLayout ws_layout(const moe_dims *d, const moe_opts *opt) {
         L.offsets = take(sizeof(int32_t) * (NB + 1));
         L.sorted_slot = take(sizeof(int32_t) * L.rcap);
         L.slot_row = take(sizeof(int32_t) * nslots);
-        // gathered token rows: only dense stages (and inputs too large for
-        // the gate/up GEMM's folded gather) read them
-        const bool xperm = opt->gemm_mode != MOE_GEMM_GROUP || !gather_foldable(*d);
+        // gathered token rows: only read when the input is too large for the
+        // gate/up GEMM's folded gather (32-bit byte offsets into x)
+        const bool xperm = !gather_foldable(*d);
         L.x_perm = take(xperm ? sizeof(bf16_t) * L.rcap * d->hidden : 0);
         L.act = take(sizeof(bf16_t) * L.rcap * d->inter);
         L.y_perm = take(sizeof(float) * L.rcap * d->hidden);
@@ -215,9 +215,9 @@ moe_status moe_ffn_group(const moe_dims *dims, int32_t e_first, int32_t e_count,
     hipStream_t s = (hipStream_t)stream;
     // no workspace here: every tile covers the whole K range in one pass
     MOE_HIP(launch_group_gateup(*dims, e_first, e_count, offsets, x_perm, nullptr, w_gate, w_up,
-                                act, grid, nullptr, nullptr, s));
+                                act, grid, nullptr, nullptr, group_tile_rows(), s));
     MOE_HIP(launch_group_down(*dims, e_first, e_count, offsets, act, w_down, y_perm, grid,
-                              nullptr, nullptr, s));
+                              nullptr, nullptr, group_tile_rows(), s));
     return MOE_OK;
 }
 
@@ -233,8 +233,10 @@ moe_status moe_ffn_dense(int64_t rows, int32_t hidden, int32_t inter, const moe_
     if (!x || !w_gate || !w_up || !w_down || !act || !y)
         return fail(MOE_ERR_INVALID, "moe_ffn_dense: NULL tensor");
     hipStream_t s = (hipStream_t)stream;
-    MOE_HIP(launch_dense_gateup(rows, hidden, inter, x, w_gate, w_up, act, s));
-    MOE_HIP(launch_dense_down(rows, hidden, inter, act, w_down, y, s));
+    // the tile height whose tile count fills the chip best for these rows
+    const int bm = dense_tile_rows(rows, hidden, inter, device_cu_count(), false);
+    MOE_HIP(launch_dense_gateup(rows, hidden, inter, x, w_gate, w_up, act, bm, s));
+    MOE_HIP(launch_dense_down(rows, hidden, inter, act, w_down, y, bm, s));
     return MOE_OK;
 }
 

@@ -130,19 +130,36 @@ hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, int64_t t
 // persistent grid may be cut along K (then a fixup kernel follows the GEMM
 // on the same stream); without them every tile is one pass over K.
 // Launches that share the scratch must not overlap.
+// bm: token rows of the tile (group_tile_rows() for a launch whose row
+// counts the host does not know; any valid_tile_rows value otherwise).
 hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
                                const int32_t *offsets, const bf16_t *x_rows,
                                const int32_t *row_map, const bf16_t *w_gate,
                                const bf16_t *w_up, bf16_t *act, int grid, float *parts,
-                               int32_t *split_meta, hipStream_t s);
+                               int32_t *split_meta, int bm, hipStream_t s);
 hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
                              const int32_t *offsets, const bf16_t *act,
                              const bf16_t *w_down, float *y_perm, int grid, float *parts,
-                             int32_t *split_meta, hipStream_t s);
-// Dense GEMMs over `rows` host-known contiguous rows.
+                             int32_t *split_meta, int bm, hipStream_t s);
+// Dense GEMMs over `rows` host-known contiguous rows, one tile per workgroup.
 hipError_t launch_dense_gateup(int64_t rows, int H, int I, const bf16_t *x, const bf16_t *w_gate,
-                               const bf16_t *w_up, bf16_t *act, hipStream_t s);
+                               const bf16_t *w_up, bf16_t *act, int bm, hipStream_t s);
 hipError_t launch_dense_down(int64_t rows, int H, int I, const bf16_t *act,
-                             const bf16_t *w_down, float *y, hipStream_t s);
+                             const bf16_t *w_down, float *y, int bm, hipStream_t s);
+
+// ---- GEMM launch-cost model (host only) ----------------------------------
+// Predicted microseconds of one persistent launch of `tiles` tiles of bm
+// token rows over K (mode 0 gate/up, 1 down) on `grid` workgroups, with or
+// without the K split of a partial last round.
+double gemm_launch_us(int mode, int bm, int64_t tiles, int K, int grid, bool split);
+// Tiles of one expert of `rows` rows: gate/up N = I (128 act columns per
+// tile), down N = H (256 per tile).
+int64_t gemm_tiles(int mode, int bm, int64_t rows, int N);
+// Gate/up + down of one expert as two dense launches.
+double ffn_expert_us(int bm, int64_t rows, int H, int I, int grid, bool split);
+// The tile height the model prefers for a dense launch of `rows` rows.
+int dense_tile_rows(int64_t rows, int H, int I, int grid, bool split);
+int group_tile_rows();
+bool valid_tile_rows(int bm);
 
 }  // namespace moe

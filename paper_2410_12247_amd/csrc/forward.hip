@@ -34,13 +34,12 @@ __global__ void shared_offsets_kernel(int32_t *__restrict__ off, int32_t T) {
     if (threadIdx.x < 2) off[threadIdx.x] = threadIdx.x == 0 ? 0 : T;
 }
 
-// AUTO's DenseGemm threshold (rows of every expert of a stage).  Measured on
-// MI355X over the skewed DeepSeekV2-shaped sweep (T = 64 .. 65536, up to
-// 58K rows on one expert) and the Mixtral / DBRX shards, the grouped launch
-// beat per-expert dense launches at every load (one tile wave tail instead
-// of one per expert, same MFMA tile), so the built-in threshold is never
-// reached; callers can lower it through moe_opts.dense_min_rows.
-constexpr int32_t kDefaultDenseMinRows = 1 << 30;
+// AUTO weighs GroupGemm against DenseGemm with the launch-cost model only
+// for stages of at most this many experts: every dense launch pays its own
+// partial round of tiles, so with more experts per stage the single grouped
+// launch wins at every load the model (and the measured sweep) covers, and
+// AUTO then needs no host copy of the row counts.
+constexpr int kAutoDenseMaxExperts = 2;
 
 enum Phase {
     PH_ROUTE, PH_PERMUTE, PH_GATHER, PH_GATEUP, PH_DOWN, PH_SHARED, PH_COMBINE, PH_TOTAL, PH_N
@@ -178,8 +177,10 @@ moe_status check_opts(const moe_dims *d, const moe_opts *o) {
     if (o->flags &
         ~(MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM | MOE_FLAG_EXACT_ORDER | MOE_FLAG_SERIAL))
         return fail(MOE_ERR_INVALID, "unknown flags 0x%x", o->flags);
-    for (int i = 0; i < 2; ++i)
-        if (o->reserved[i]) return fail(MOE_ERR_INVALID, "reserved options must be zero");
+    if (o->dense_tile_rows != 0 && !valid_tile_rows(o->dense_tile_rows))
+        return fail(MOE_ERR_INVALID, "dense_tile_rows %d is not 0, 128, 192, 256 or 320",
+                    o->dense_tile_rows);
+    if (o->reserved[0]) return fail(MOE_ERR_INVALID, "reserved options must be zero");
     return MOE_OK;
 }
 
@@ -190,13 +191,50 @@ int forward_buckets(const moe_dims *d, const moe_opts *o) {
     return o->chunk_mode == MOE_CHUNK_TOKENS ? o->pipeline_n * d->local_count : d->local_count;
 }
 
+// Experts per pipeline stage.
+int stage_experts(const moe_dims &d, const moe_opts &o) {
+    return o.chunk_mode == MOE_CHUNK_TOKENS ? d.local_count : d.local_count / o.pipeline_n;
+}
+
 bool needs_host_counts(const moe_dims &d, const moe_opts &o) {
-    const int32_t m_star = o.dense_min_rows > 0 ? o.dense_min_rows : kDefaultDenseMinRows;
     // row counts are needed on the host to size per-expert dense launches and
-    // stage gathers; AUTO is GROUP without a sync when no expert can reach the
-    // threshold (an expert has at most T rows) and PN = 1
-    return o.gemm_mode == MOE_GEMM_DENSE || o.pipeline_n > 1 ||
-           (o.gemm_mode == MOE_GEMM_AUTO && m_star <= d.tokens);
+    // stage gathers, and for AUTO to weigh the two GEMM kinds: with a fixed
+    // threshold only when some expert can reach it (an expert has at most T
+    // rows), with the cost model only for stages of few experts
+    if (o.gemm_mode == MOE_GEMM_DENSE || o.pipeline_n > 1) return true;
+    if (o.gemm_mode != MOE_GEMM_AUTO) return false;
+    if (o.dense_min_rows > 0) return o.dense_min_rows <= d.tokens;
+    return stage_experts(d, o) <= kAutoDenseMaxExperts;
+}
+
+// AUTO's choice for one stage of n experts with host row counts `rows`:
+// DenseGemm (one launch per expert, tile height from its rows) when the
+// launch-cost model predicts it faster than one grouped launch over the
+// stage (or, with a fixed threshold m*, when every expert has >= m* rows).
+bool auto_picks_dense(const moe_dims &d, const moe_opts &o, const int32_t *rows, int n, int grid,
+                      bool split, double *group_us, double *dense_us) {
+    const int bm_g = group_tile_rows();
+    int64_t tiles_gu = 0, tiles_dn = 0;
+    double dus = 0.0;
+    int32_t min_rows = INT32_MAX;
+    for (int e = 0; e < n; ++e) {
+        tiles_gu += gemm_tiles(0, bm_g, rows[e], d.inter);
+        tiles_dn += gemm_tiles(1, bm_g, rows[e], d.hidden);
+        min_rows = std::min(min_rows, rows[e]);
+        if (rows[e] > 0) {
+            const int bm = o.dense_tile_rows > 0
+                               ? o.dense_tile_rows
+                               : dense_tile_rows(rows[e], d.hidden, d.inter, grid, split);
+            dus += ffn_expert_us(bm, rows[e], d.hidden, d.inter, grid, split);
+        }
+    }
+    const double gus = gemm_launch_us(0, bm_g, tiles_gu, d.hidden, grid, split) +
+                       gemm_launch_us(1, bm_g, tiles_dn, d.inter, grid, split);
+    if (group_us) *group_us = gus;
+    if (dense_us) *dense_us = dus;
+    if (o.dense_min_rows > 0) return min_rows >= o.dense_min_rows;
+    if (n > kAutoDenseMaxExperts) return false;
+    return dus < gus;
 }
 
 // Scratch of the no-allocation entry point: one static buffer per device
@@ -334,9 +372,10 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         shared_offsets_kernel<<<1, 64, 0, sm>>>(soff, (int32_t)T);
         MOE_HIP(hipGetLastError());
         MOE_HIP(launch_group_gateup(ds, 0, 1, soff, x, nullptr, shared_gate, shared_up,
-                                    shared_act, grid, split_part, split_meta, sm));
+                                    shared_act, grid, split_part, split_meta, group_tile_rows(),
+                                    sm));
         MOE_HIP(launch_group_down(ds, 0, 1, soff, shared_act, shared_down, y, grid, split_part,
-                                  split_meta, sm));
+                                  split_meta, group_tile_rows(), sm));
         MOE_TRY(tm.end(sm));
     }
 
@@ -351,10 +390,6 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
 
     // GEMM kind per stage needs the row counts on the host
     std::vector<int32_t> hc;
-    const int32_t m_star = o->dense_min_rows > 0 ? o->dense_min_rows : kDefaultDenseMinRows;
-    // row counts are needed on the host to size per-expert dense launches and
-    // stage gathers; AUTO is GROUP without a sync when no expert can reach the
-    // threshold (an expert has at most T rows) and PN = 1
     const bool need_counts = needs_host_counts(d, *o);
     if (need_counts) {
         if (!st) return fail(MOE_ERR_UNSUPPORTED, "row counts needed on the host");
@@ -387,16 +422,14 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         bool dense = o->gemm_mode == MOE_GEMM_DENSE;
         if (need_counts) {
             stage_rows = 0;
-            int32_t min_rows = INT32_MAX;
-            for (int b = b0; b < b0 + per_stage; ++b) {
-                stage_rows += hc[b];
-                min_rows = std::min(min_rows, hc[b]);
-            }
-            if (o->gemm_mode == MOE_GEMM_AUTO) dense = min_rows >= m_star;
+            for (int b = b0; b < b0 + per_stage; ++b) stage_rows += hc[b];
+            if (o->gemm_mode == MOE_GEMM_AUTO)
+                dense = auto_picks_dense(d, *o, &hc[b0], per_stage, grid, split, nullptr,
+                                         nullptr);
         }
-        // gather (dispatch of this stage); a grouped stage reads its token
-        // rows straight from x through sorted_slot instead
-        const bool fold_gather = !dense && fold_ok;
+        // gather (dispatch of this stage), unless the gate/up GEMM reads its
+        // token rows straight from x through sorted_slot
+        const bool fold_gather = fold_ok;
         if (!fold_gather) {
             MOE_TRY(tm.begin(sg, PH_GATHER));
             MOE_HIP(launch_gather(d, b0, per_stage, off, sorted_slot, x, x_perm, stage_rows,
@@ -409,44 +442,48 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
             tm.gap();
         }
 
-        // expert GEMMs
+        // expert GEMMs; the grouped kernels index weights from their first
+        // expert: the offsets are shifted so that expert e_w .. is bucket b0 ..
+        const int32_t *goff = off + (b0 - e_w);
+        const bf16_t *xrows = fold_gather ? x : x_perm;
+        const int32_t *rmap = fold_gather ? sorted_slot : nullptr;
         if (dense) {
+            // DenseGemm: one launch per expert, whose row count the host
+            // knows, so each takes the tile height that fills the grid best
             if (timing) ++g_timing.dense_stages;
-            int64_t r0 = 0;
-            for (int b = 0; b < b0; ++b) r0 += hc[b];
             for (int b = b0; b < b0 + per_stage; ++b) {
                 const int64_t rows = hc[b];
-                if (rows > 0) {
-                    const int64_t wo = (int64_t)(e_w + b - b0) * I * H;
-                    MOE_TRY(tm.begin(sm, PH_GATEUP));
-                    MOE_HIP(launch_dense_gateup(rows, H, I, x_perm + r0 * H, w_gate + wo,
-                                                w_up + wo, act + r0 * I, sm));
-                    MOE_TRY(tm.end(sm));
-                    MOE_TRY(tm.begin(sm, PH_DOWN));
-                    MOE_HIP(launch_dense_down(rows, H, I, act + r0 * I, w_down + wo,
-                                              y_perm + r0 * H, sm));
-                    MOE_TRY(tm.end(sm));
-                    if (timing) {
-                        ++g_timing.gateup_launches;
-                        ++g_timing.down_launches;
-                    }
+                if (rows <= 0) continue;
+                const int e = e_w + (b - b0);
+                const int bm = o->dense_tile_rows > 0
+                                   ? o->dense_tile_rows
+                                   : dense_tile_rows(rows, H, I, grid, split);
+                MOE_TRY(tm.begin(sm, PH_GATEUP));
+                MOE_HIP(launch_group_gateup(d, e, 1, goff, xrows, rmap, w_gate, w_up, act, grid,
+                                            split_part, split_meta, bm, sm));
+                MOE_TRY(tm.end(sm));
+                MOE_TRY(tm.begin(sm, PH_DOWN));
+                MOE_HIP(launch_group_down(d, e, 1, goff, act, w_down, y_perm, grid, split_part,
+                                          split_meta, bm, sm));
+                MOE_TRY(tm.end(sm));
+                if (timing) {
+                    ++g_timing.gateup_launches;
+                    ++g_timing.down_launches;
                 }
-                r0 += rows;
             }
         } else {
+            // GroupGemm: one launch over the stage's experts, row counts
+            // read on the device
             if (timing) ++g_timing.group_stages;
             if (stage_rows > 0) {
-                // the grouped kernels index weights from their first expert:
-                // shift the offsets so that expert e_w .. is bucket b0 ..
-                const int32_t *goff = off + (b0 - e_w);
+                const int bm = group_tile_rows();
                 MOE_TRY(tm.begin(sm, PH_GATEUP));
-                MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, fold_gather ? x : x_perm,
-                                            fold_gather ? sorted_slot : nullptr, w_gate, w_up,
-                                            act, grid, split_part, split_meta, sm));
+                MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, xrows, rmap, w_gate, w_up,
+                                            act, grid, split_part, split_meta, bm, sm));
                 MOE_TRY(tm.end(sm));
                 MOE_TRY(tm.begin(sm, PH_DOWN));
                 MOE_HIP(launch_group_down(d, e_w, per_stage, goff, act, w_down, y_perm, grid,
-                                          split_part, split_meta, sm));
+                                          split_part, split_meta, bm, sm));
                 MOE_TRY(tm.end(sm));
                 if (timing) {
                     ++g_timing.gateup_launches;
@@ -484,7 +521,36 @@ using namespace moe;
 
 extern "C" {
 
-int32_t moe_default_dense_min_rows(void) { return kDefaultDenseMinRows; }
+moe_status moe_gemm_plan(const moe_dims *dims, const moe_opts *opts, int32_t n_experts,
+                         const int32_t *rows, int32_t *dense, int32_t *tile_rows,
+                         double *group_us, double *dense_us) {
+    MOE_TRY(check_dims(dims));
+    moe_opts defaults{};
+    defaults.pipeline_n = 1;
+    const moe_opts *o = opts ? opts : &defaults;
+    MOE_TRY(check_opts(dims, o));
+    if (n_experts < 1 || n_experts > kMaxExperts)
+        return fail(MOE_ERR_INVALID, "moe_gemm_plan: n_experts %d outside [1, %d]", n_experts,
+                    kMaxExperts);
+    if (!rows || !dense) return fail(MOE_ERR_INVALID, "moe_gemm_plan: NULL rows or dense");
+    for (int e = 0; e < n_experts; ++e)
+        if (rows[e] < 0) return fail(MOE_ERR_INVALID, "moe_gemm_plan: rows[%d] < 0", e);
+    int grid = o->gemm_cu_budget > 0 ? o->gemm_cu_budget : device_cu_count();
+    grid = std::max(8, (grid / 8) * 8);
+    const bool split = (o->flags & MOE_FLAG_EXACT_ORDER) == 0;
+    bool d_ = auto_picks_dense(*dims, *o, rows, n_experts, grid, split, group_us, dense_us);
+    if (o->gemm_mode == MOE_GEMM_GROUP) d_ = false;
+    if (o->gemm_mode == MOE_GEMM_DENSE) d_ = true;
+    *dense = d_ ? 1 : 0;
+    if (tile_rows)
+        for (int e = 0; e < n_experts; ++e)
+            tile_rows[e] = !d_ ? group_tile_rows()
+                           : rows[e] == 0 ? 0
+                           : o->dense_tile_rows > 0
+                               ? o->dense_tile_rows
+                               : dense_tile_rows(rows[e], dims->hidden, dims->inter, grid, split);
+    return MOE_OK;
+}
 
 // The pipeline-number model of the paper's ablation (Sec. 5.2): the overlap
 // hides C/PN of each of PN - 1 stages, and cutting the work costs

@@ -873,49 +873,24 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(const float *__restric
     }
 }
 
-// Tile policy of each scheduler.
+// Tile policy of each scheduler: the ping-pong tile, 256 weight rows by BM
+// token rows.  The grouped launch does not know its row counts on the host
+// and always takes the tallest tile (BM = 320, fewest LDS bytes per MFMA);
+// a dense launch knows its expert's rows and takes the height whose tile
+// count fills the grid best (dense_tile_rows).
 #ifndef MOE_GEMM_PINGPONG
 #define MOE_GEMM_PINGPONG 1
 #endif
 #if MOE_GEMM_PINGPONG
 constexpr int kTokenTile = 320;
-template <int MODE> using DenseTile = PingPong<MODE, kTokenTile>;
-template <int MODE> using GroupTile = PingPong<MODE, kTokenTile>;
+template <int MODE, int BM = kTokenTile> using TileOf = PingPong<MODE, BM>;
 #else
-template <int MODE> using DenseTile = FourWave<MODE, 256, 256, 32, 4>;
-template <int MODE> using GroupTile = FourWave<MODE, 256, 256, 32, 4>;
+constexpr int kTokenTile = 256;
+template <int MODE, int BM = kTokenTile> using TileOf = FourWave<MODE, 256, 256, 32, 4>;
 #endif
+template <int MODE> using GroupTile = TileOf<MODE>;
 
 int round_grid(int64_t tiles) { return (int)(((tiles + NXCD - 1) / NXCD) * NXCD); }
-
-}  // namespace
-
-hipError_t launch_dense_gateup(int64_t rows, int H, int I, const bf16_t *x, const bf16_t *w_gate,
-                               const bf16_t *w_up, bf16_t *act, hipStream_t s) {
-    if (rows <= 0) return hipSuccess;
-    using TP = DenseTile<0>;
-    const int MT = (int)((rows + TP::BM - 1) / TP::BM);
-    const int NT = (I + TP::BNOUT - 1) / TP::BNOUT;
-    dense_kernel<0, TP><<<round_grid((int64_t)MT * NT), TP::THREADS, 0, s>>>(
-        x, rows, w_gate, w_up, I, H, act, I, MT, NT);
-    return hipGetLastError();
-}
-
-hipError_t launch_dense_down(int64_t rows, int H, int I, const bf16_t *act,
-                             const bf16_t *w_down, float *y, hipStream_t s) {
-    if (rows <= 0) return hipSuccess;
-    using TP = DenseTile<1>;
-    const int MT = (int)((rows + TP::BM - 1) / TP::BM);
-    const int NT = (H + TP::BNOUT - 1) / TP::BNOUT;
-    dense_kernel<1, TP><<<round_grid((int64_t)MT * NT), TP::THREADS, 0, s>>>(
-        act, rows, w_down, nullptr, H, I, y, H, MT, NT);
-    return hipGetLastError();
-}
-
-size_t gemm_split_bytes() {
-    const size_t e = std::max(GroupTile<0>::PART_ELEMS, GroupTile<1>::PART_ELEMS);
-    return e * sizeof(float) * kSplitSlots;
-}
 
 // Fixup launch after a grouped GEMM that was given a split buffer: at most
 // min(grid, kSplitSlots) / 2 tiles can be cut (each into two or more
@@ -934,35 +909,207 @@ hipError_t launch_split_fixup(int grid, const float *parts, const int32_t *meta,
     }
 }
 
+template <int MODE, class TP>
+hipError_t group_launch(const int32_t *offsets, int e_first, int e_count, const bf16_t *x,
+                        const int32_t *row_map, int slot_div, const bf16_t *w0s,
+                        const bf16_t *w1s, int64_t wstride, int N, int K, void *out,
+                        int64_t ldo, int grid, float *parts, int32_t *split_meta, hipStream_t s) {
+    const bool split = parts != nullptr && split_meta != nullptr;
+    group_kernel<MODE, TP><<<grid, TP::THREADS, 0, s>>>(
+        offsets, e_first, e_count, x, row_map, slot_div, w0s, w1s, wstride, N, K, out, ldo,
+        split ? parts : nullptr, split ? split_meta : nullptr);
+    if (split) return launch_split_fixup<MODE, TP>(grid, parts, split_meta, out, ldo, s);
+    return hipGetLastError();
+}
+
+template <int MODE>
+hipError_t group_launch_bm(int bm, const int32_t *offsets, int e_first, int e_count,
+                           const bf16_t *x, const int32_t *row_map, int slot_div,
+                           const bf16_t *w0s, const bf16_t *w1s, int64_t wstride, int N, int K,
+                           void *out, int64_t ldo, int grid, float *parts, int32_t *split_meta,
+                           hipStream_t s) {
+#define MOE_GROUP_LAUNCH(BMV)                                                                   \
+    return group_launch<MODE, TileOf<MODE, BMV>>(offsets, e_first, e_count, x, row_map,       \
+                                                 slot_div, w0s, w1s, wstride, N, K, out, ldo, \
+                                                 grid, parts, split_meta, s)
+#if MOE_GEMM_PINGPONG
+    switch (bm) {
+        case 128: MOE_GROUP_LAUNCH(128);
+        case 192: MOE_GROUP_LAUNCH(192);
+        case 256: MOE_GROUP_LAUNCH(256);
+        default: MOE_GROUP_LAUNCH(320);
+    }
+#else
+    MOE_GROUP_LAUNCH(256);
+#endif
+#undef MOE_GROUP_LAUNCH
+}
+
+template <int MODE, class TP>
+hipError_t dense_launch(int64_t rows, const bf16_t *x, const bf16_t *w0, const bf16_t *w1, int N,
+                        int K, void *out, int64_t ldo, hipStream_t s) {
+    const int MT = (int)((rows + TP::BM - 1) / TP::BM);
+    const int NT = (N + TP::BNOUT - 1) / TP::BNOUT;
+    dense_kernel<MODE, TP><<<round_grid((int64_t)MT * NT), TP::THREADS, 0, s>>>(
+        x, rows, w0, w1, N, K, out, ldo, MT, NT);
+    return hipGetLastError();
+}
+
+template <int MODE>
+hipError_t dense_launch_bm(int bm, int64_t rows, const bf16_t *x, const bf16_t *w0,
+                           const bf16_t *w1, int N, int K, void *out, int64_t ldo, hipStream_t s) {
+#if MOE_GEMM_PINGPONG
+    switch (bm) {
+        case 128: return dense_launch<MODE, TileOf<MODE, 128>>(rows, x, w0, w1, N, K, out, ldo, s);
+        case 192: return dense_launch<MODE, TileOf<MODE, 192>>(rows, x, w0, w1, N, K, out, ldo, s);
+        case 256: return dense_launch<MODE, TileOf<MODE, 256>>(rows, x, w0, w1, N, K, out, ldo, s);
+        default: return dense_launch<MODE, TileOf<MODE, 320>>(rows, x, w0, w1, N, K, out, ldo, s);
+    }
+#else
+    return dense_launch<MODE, TileOf<MODE>>(rows, x, w0, w1, N, K, out, ldo, s);
+#endif
+}
+
+// ---- launch cost model (host) ---------------------------------------------
+// Device time of one launch of the persistent scheduler, from per-tile costs
+// of each tile height measured on MI355X (microseconds):
+//   tile time = nk * step(MODE, BM) + epi(MODE, BM)
+// where nk is the number of 32-deep K stages.  Tiles run in rounds of G
+// workgroups; a partial round of rem tiles takes the fraction
+// kPartialRound[MODE] + (1 - kPartialRound) * busy of a full round's K loop
+// (busy = the fraction of workgroups with work: fewer active compute units
+// run each tile faster), then the epilogue.  With the K split, a partial
+// last round of rem <= G/2 tiles is cut into S pieces as the scheduler does
+// (S = min(8, G/rem, nk/32, slots/rem)): its K loop is S times shorter, and
+// the fixup costs a fixed time plus a time per partial-sum block (its bytes
+// grow with BM).  Each launch pays a fixed start-up and drain time.
+struct TileCost {
+    int bm;
+    double step_us[2];  // one 32-deep K stage of a 256 x BM tile: gate/up, down
+    double epi_us[2];   // a tile's epilogue: gate/up (bf16 SiLU*mul), down (fp32)
+};
+// Fitted by least squares (4.5% rms, 14% worst) to one expert's dense
+// launches at 512 .. 32768 rows on the DeepSeekV2 (H 5120, I 1536) and
+// Mixtral (H 4096, I 3584) expert shapes, every tile height, with and
+// without the K split (bench.py --tile-study).
+constexpr TileCost kTileCosts[] = {
+    {320, {0.912, 0.995}, {10.4, 10.9}},
+    {256, {0.757, 0.832}, {11.6, 11.9}},
+    {192, {0.630, 0.699}, {6.0, 8.2}},
+    {128, {0.557, 0.561}, {0.0, 7.4}},
+};
+constexpr double kLaunchUs[2] = {13.5, 7.5};     // start-up + drain: gate/up, down
+constexpr double kPartialRound[2] = {0.71, 0.72};
+constexpr double kFixupUs[2] = {4.7, 2.2};       // fixup launch with work
+constexpr double kFixupBlockUs[2] = {0.0795, 0.0741};  // per 256 x 320 partial block
+
+const TileCost &tile_cost(int bm) {
+    for (const TileCost &c : kTileCosts)
+        if (c.bm == bm) return c;
+    return kTileCosts[0];
+}
+
+}  // namespace
+
+double gemm_launch_us(int mode, int bm, int64_t tiles, int K, int grid, bool split) {
+    if (tiles <= 0) return 0.0;
+    const TileCost &c = tile_cost(bm);
+    const int md = mode ? 1 : 0;
+    const int nk = K / 32;
+    const double loop_us = nk * c.step_us[md];
+    const int64_t full_rounds = tiles / grid;
+    const int64_t rem = tiles % grid;
+    double us = kLaunchUs[md] + full_rounds * (loop_us + c.epi_us[md]);
+    if (rem > 0) {
+        int S = 1;
+        if (split && 2 * rem <= grid)
+            S = (int)std::min<int64_t>(std::min<int64_t>(kSplitMaxPieces, grid / rem),
+                                       std::min<int64_t>(nk / kSplitMinStages, kSplitSlots / rem));
+        const double busy = (double)std::min<int64_t>(grid, rem * std::max(S, 1)) / grid;
+        const double part = kPartialRound[md] + (1.0 - kPartialRound[md]) * busy;
+        if (S >= 2)
+            us += loop_us / S * part + c.epi_us[md] + kFixupUs[md] +
+                  kFixupBlockUs[md] * (double)(rem * S) * bm / 320.0;
+        else
+            us += loop_us * part + c.epi_us[md];
+    }
+    return us;
+}
+
+int64_t gemm_tiles(int mode, int bm, int64_t rows, int N) {
+    const int bnout = mode == 0 ? 128 : 256;
+    return ((rows + bm - 1) / bm) * ((N + bnout - 1) / bnout);
+}
+
+double ffn_expert_us(int bm, int64_t rows, int H, int I, int grid, bool split) {
+    return gemm_launch_us(0, bm, gemm_tiles(0, bm, rows, I), H, grid, split) +
+           gemm_launch_us(1, bm, gemm_tiles(1, bm, rows, H), I, grid, split);
+}
+
+int dense_tile_rows(int64_t rows, int H, int I, int grid, bool split) {
+#if MOE_GEMM_PINGPONG
+    int best = kTokenTile;
+    double best_us = 0.0;
+    for (const TileCost &c : kTileCosts) {
+        const double us = ffn_expert_us(c.bm, rows, H, I, grid, split);
+        if (best_us == 0.0 || us < best_us) {
+            best = c.bm;
+            best_us = us;
+        }
+    }
+    return best;
+#else
+    return kTokenTile;
+#endif
+}
+
+int group_tile_rows() { return kTokenTile; }
+
+bool valid_tile_rows(int bm) {
+#if MOE_GEMM_PINGPONG
+    return bm == 128 || bm == 192 || bm == 256 || bm == 320;
+#else
+    return bm == kTokenTile;
+#endif
+}
+
+hipError_t launch_dense_gateup(int64_t rows, int H, int I, const bf16_t *x, const bf16_t *w_gate,
+                               const bf16_t *w_up, bf16_t *act, int bm, hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    return dense_launch_bm<0>(bm, rows, x, w_gate, w_up, I, H, act, I, s);
+}
+
+hipError_t launch_dense_down(int64_t rows, int H, int I, const bf16_t *act,
+                             const bf16_t *w_down, float *y, int bm, hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    return dense_launch_bm<1>(bm, rows, act, w_down, nullptr, H, I, y, H, s);
+}
+
+size_t gemm_split_bytes() {
+    // the tallest tile has the largest block of partial sums
+    const size_t e = std::max(GroupTile<0>::PART_ELEMS, GroupTile<1>::PART_ELEMS);
+    return e * sizeof(float) * kSplitSlots;
+}
+
 hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
                                const int32_t *offsets, const bf16_t *x_rows,
                                const int32_t *row_map, const bf16_t *w_gate,
                                const bf16_t *w_up, bf16_t *act, int grid, float *parts,
-                               int32_t *split_meta, hipStream_t s) {
+                               int32_t *split_meta, int bm, hipStream_t s) {
     if (e_count <= 0) return hipSuccess;
-    using TP = GroupTile<0>;
-    const bool split = parts != nullptr && split_meta != nullptr;
-    group_kernel<0, TP><<<grid, TP::THREADS, 0, s>>>(
-        offsets, e_first, e_count, x_rows, row_map, d.top_k, w_gate, w_up,
-        (int64_t)d.inter * d.hidden, d.inter, d.hidden, act, d.inter,
-        split ? parts : nullptr, split ? split_meta : nullptr);
-    if (split) return launch_split_fixup<0, TP>(grid, parts, split_meta, act, d.inter, s);
-    return hipGetLastError();
+    return group_launch_bm<0>(bm, offsets, e_first, e_count, x_rows, row_map, d.top_k, w_gate,
+                              w_up, (int64_t)d.inter * d.hidden, d.inter, d.hidden, act,
+                              d.inter, grid, parts, split_meta, s);
 }
 
 hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
                              const int32_t *offsets, const bf16_t *act,
                              const bf16_t *w_down, float *y_perm, int grid, float *parts,
-                             int32_t *split_meta, hipStream_t s) {
+                             int32_t *split_meta, int bm, hipStream_t s) {
     if (e_count <= 0) return hipSuccess;
-    using TP = GroupTile<1>;
-    const bool split = parts != nullptr && split_meta != nullptr;
-    group_kernel<1, TP><<<grid, TP::THREADS, 0, s>>>(
-        offsets, e_first, e_count, act, nullptr, 1, w_down, nullptr,
-        (int64_t)d.hidden * d.inter, d.hidden, d.inter, y_perm, d.hidden,
-        split ? parts : nullptr, split ? split_meta : nullptr);
-    if (split) return launch_split_fixup<1, TP>(grid, parts, split_meta, y_perm, d.hidden, s);
-    return hipGetLastError();
+    return group_launch_bm<1>(bm, offsets, e_first, e_count, act, nullptr, 1, w_down, nullptr,
+                              (int64_t)d.hidden * d.inter, d.hidden, d.inter, y_perm, d.hidden,
+                              grid, parts, split_meta, s);
 }
 
 }  // namespace moe

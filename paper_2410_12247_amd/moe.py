@@ -24,7 +24,7 @@ FLAG_TIMING, FLAG_TIMING_GEMM, FLAG_EXACT_ORDER, FLAG_SERIAL = 1, 2, 4, 8
 EXPORTS = ("moe_workspace_bytes", "moe_route", "moe_permute", "moe_gather", "moe_ffn_group",
            "moe_ffn_dense", "moe_combine", "moe_ffn_forward", "moe_ffn_forward_noalloc",
            "moe_last_timing",
-           "moe_default_dense_min_rows", "moe_choose_pipeline_n", "moe_status_string",
+           "moe_gemm_plan", "moe_choose_pipeline_n", "moe_status_string",
            "moe_last_error")
 
 
@@ -46,7 +46,7 @@ class Opts(ctypes.Structure):
     _fields_ = [("gemm_mode", ctypes.c_int32), ("dense_min_rows", ctypes.c_int32),
                 ("pipeline_n", ctypes.c_int32), ("gemm_cu_budget", ctypes.c_int32),
                 ("flags", ctypes.c_int32), ("chunk_mode", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 2)]
+                ("dense_tile_rows", ctypes.c_int32), ("reserved", ctypes.c_int32 * 1)]
 
 
 class Timing(ctypes.Structure):
@@ -82,7 +82,8 @@ def lib():
     L.moe_ffn_forward.argtypes = [D, O, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
     L.moe_ffn_forward_noalloc.argtypes = [D, O, P, P, P, P, P, P, P, P, P, P, P, P, P, P]
     L.moe_last_timing.argtypes = [ctypes.POINTER(Timing)]
-    L.moe_default_dense_min_rows.restype = I32
+    L.moe_gemm_plan.argtypes = [D, O, I32, P, ctypes.POINTER(I32), P,
+                                ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     L.moe_choose_pipeline_n.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double, I32,
                                         ctypes.POINTER(I32), ctypes.POINTER(ctypes.c_double)]
     L.moe_status_string.argtypes = [I32]
@@ -90,7 +91,7 @@ def lib():
     L.moe_last_error.restype = ctypes.c_char_p
     for name in ("moe_route", "moe_permute", "moe_gather", "moe_ffn_group", "moe_ffn_dense",
                  "moe_combine", "moe_ffn_forward", "moe_ffn_forward_noalloc", "moe_last_timing",
-                 "moe_choose_pipeline_n"):
+                 "moe_choose_pipeline_n", "moe_gemm_plan"):
         getattr(L, name).restype = I32
     _lib = L
     return L
@@ -111,7 +112,8 @@ def dims(tokens, hidden, inter, experts, top_k, local_begin=0, local_count=None,
 
 
 def opts(gemm_mode=GEMM_AUTO, dense_min_rows=0, pipeline_n=1, gemm_cu_budget=0,
-         timing=False, chunk_mode=CHUNK_EXPERTS, exact_order=False, serial=False) -> Opts:
+         timing=False, chunk_mode=CHUNK_EXPERTS, exact_order=False, serial=False,
+         dense_tile_rows=0) -> Opts:
     """timing: False, True (every phase) or "gemm" (the GEMM launches only).
     exact_order: no K split of the grouped GEMM's last round (the same bits
     for every pipeline number, stage kind, CU budget and GEMM kind).
@@ -125,6 +127,7 @@ def opts(gemm_mode=GEMM_AUTO, dense_min_rows=0, pipeline_n=1, gemm_cu_budget=0,
     if serial:
         o.flags |= FLAG_SERIAL
     o.chunk_mode = chunk_mode
+    o.dense_tile_rows = dense_tile_rows
     return o
 
 
@@ -213,8 +216,19 @@ def last_timing() -> dict:
     return t.as_dict()
 
 
-def default_dense_min_rows() -> int:
-    return lib().moe_default_dense_min_rows()
+def gemm_plan(d: Dims, o: Optional[Opts], rows):
+    """AUTO's plan for one stage with host row counts `rows`: (dense, tile
+    rows per expert, predicted group us, predicted dense us)."""
+    import numpy as np
+    r = np.ascontiguousarray(rows, dtype=np.int32)
+    tiles = np.zeros(len(r), np.int32)
+    dense = ctypes.c_int32()
+    gus, dus = ctypes.c_double(), ctypes.c_double()
+    _check(lib().moe_gemm_plan(ctypes.byref(d), ctypes.byref(o) if o is not None else None,
+                               len(r), r.ctypes.data_as(ctypes.c_void_p), ctypes.byref(dense),
+                               tiles.ctypes.data_as(ctypes.c_void_p), ctypes.byref(gus),
+                               ctypes.byref(dus)))
+    return bool(dense.value), tiles.tolist(), gus.value, dus.value
 
 
 class MoEBuffers:

@@ -40,8 +40,8 @@ def test_workspace_bytes_host_only():
     pm = moe.workspace_bytes(d)
     assert 0 < pm < fw
     R = 16384 * 2
-    # forward workspace holds x_perm (bf16), act (bf16) and y_perm (fp32) rows
-    assert fw >= R * (4096 * 2 + 3584 * 2 + 4096 * 4)
+    # forward workspace holds act (bf16) and y_perm (fp32) rows
+    assert fw >= R * (3584 * 2 + 4096 * 4)
     assert moe.workspace_bytes(moe.dims(16, 100, 64, 8, 2), moe.opts()) == 0  # H % 64
 
 
@@ -112,7 +112,7 @@ def test_invalid_options_and_buffers_rejected():
     assert moe.opts(exact_order=True).flags == 4
     assert moe.opts(timing="gemm", exact_order=True).flags == 6
     o = moe.opts()
-    o.reserved[1] = 5
+    o.reserved[0] = 5
     st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake, fake,
                            None, None, None, fake, None, None, None, fake, 1 << 40, None)
     assert st == 1
@@ -187,17 +187,21 @@ def test_pipeline_n_chooser_model():
 
 
 def test_workspace_holds_only_what_the_options_use():
-    """Gathered rows only when a stage may run DenseGemm (or the gather cannot
-    be folded into the GEMM), K-split partials only when the grouped GEMM may
-    cut tiles."""
+    """Gathered rows only when the GEMM cannot read token rows straight from x
+    (T * H * 2 bytes reach 2^32), K-split partials only when a GEMM may cut
+    tiles."""
     d = moe.dims(16384, 4096, 3584, 8, 2)
     R = 16384 * 2
     auto = moe.workspace_bytes(d, moe.opts())
     group = moe.workspace_bytes(d, moe.opts(gemm_mode=moe.GEMM_GROUP))
     exact = moe.workspace_bytes(d, moe.opts(gemm_mode=moe.GEMM_GROUP, exact_order=True))
-    assert auto - group >= R * 4096 * 2                      # x_perm [R][H] bf16
+    assert auto == group
     assert group - exact >= 256 * 256 * 320 * 4              # 256 partial tiles of fp32
     assert exact >= R * (3584 * 2 + 4096 * 4)                # act + y_perm
+    assert exact < R * (3584 * 2 + 4096 * 4) + R * 4096      # no x_perm [R][H] bf16
+    big = moe.dims(600000, 4096, 64, 8, 1)                   # 4.9 GB of x
+    nb = moe.workspace_bytes(big, moe.opts(exact_order=True))
+    assert nb >= 600000 * 4096 * (2 + 4)                     # x_perm + y_perm
 
 
 def test_noalloc_forward_rejects_on_the_host():
@@ -225,3 +229,45 @@ def test_noalloc_forward_rejects_on_the_host():
                                      fake, None, None, None, fake, None, None, None, None) == 1
     zero = moe.dims(0, 256, 128, 8, 2)
     assert call(zero, moe.opts()) == 0
+
+
+def test_gemm_plan_model():
+    """AUTO's GroupGemm / DenseGemm plan for one stage (moe_gemm_plan, host
+    only): forced modes, per-expert tile heights among the built ones, an
+    empty expert, the fixed threshold, and the model's choices on the shapes
+    whose measurements set it."""
+    L = moe.lib()
+    d = moe.dims(16384, 5120, 1536, 160, 6, 0, 20, False)
+    plan = moe.gemm_plan
+    # one expert of 4096 rows, DeepSeekV2 expert shape: 320-row tiles leave
+    # 156 of 256 workgroups busy for gate/up; a dense launch picks its height
+    dense, tiles, gus, dus = plan(d, moe.opts(), [4096])
+    assert tiles[0] in (128, 192, 256, 320)
+    assert dense == (dus < gus)
+    # forced kinds
+    assert plan(d, moe.opts(gemm_mode=moe.GEMM_GROUP), [4096])[:2] == (False, [320])
+    dense, tiles, _, _ = plan(d, moe.opts(gemm_mode=moe.GEMM_DENSE), [4096, 0, 17])
+    assert dense and tiles[1] == 0 and tiles[0] > 0 and tiles[2] > 0
+    dense, tiles, _, _ = plan(d, moe.opts(gemm_mode=moe.GEMM_DENSE, dense_tile_rows=192),
+                              [4096, 5])
+    assert tiles == [192, 192]
+    # many experts per stage: always one grouped launch under AUTO
+    assert plan(d, moe.opts(), [600] * 20)[0] is False
+    # the fixed threshold of Sec. 3.2: dense iff every expert reaches m
+    assert plan(d, moe.opts(dense_min_rows=1000), [1200, 3000])[0] is True
+    assert plan(d, moe.opts(dense_min_rows=1000), [999, 3000])[0] is False
+    # predicted times grow with the load
+    g1, d1 = plan(d, moe.opts(), [1024])[2:]
+    g2, d2 = plan(d, moe.opts(), [8192])[2:]
+    assert 0 < g1 < g2 and 0 < d1 < d2
+    # invalid arguments
+    with pytest.raises(moe.MoEError):
+        plan(d, moe.opts(), [-1])
+    with pytest.raises(moe.MoEError):
+        plan(d, moe.opts(dense_tile_rows=100), [10])
+    r = (ctypes.c_int32 * 1)(5)
+    out = ctypes.c_int32()
+    assert L.moe_gemm_plan(ctypes.byref(d), None, 0, r, ctypes.byref(out), None, None,
+                           None) == 1
+    assert L.moe_gemm_plan(ctypes.byref(d), None, 1, None, ctypes.byref(out), None, None,
+                           None) == 1

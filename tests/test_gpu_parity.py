@@ -294,6 +294,28 @@ def test_forward_timing_modes(name):
             assert t_gemm["shared_ms"] > 0
 
 
+@pytest.mark.parametrize("name", ["tall4", "ragged8", "window"])
+def test_dense_tile_heights(name):
+    """DenseGemm launches with every tile height (128, 192, 256, 320 token
+    rows, forced, and the one the launch-cost model picks): the same bits as
+    GroupGemm in exact order, and within the oracle bar with the K split."""
+    inp, ids, w = case(name)
+    g = Dev(inp)
+    s = inp.shape
+    base = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP, exact_order=True)).y.clone()
+    ref = oracle_y(inp, ids, w, np.arange(s.T))
+    for bm in (0, 128, 192, 256, 320):
+        for pn in (1, s.EL):
+            y = g.forward(moe.opts(gemm_mode=moe.GEMM_DENSE, dense_tile_rows=bm, pipeline_n=pn,
+                                   exact_order=True)).y
+            assert torch.equal(y, base), f"dense tile {bm} PN={pn} changes the bits"
+        y = g.forward(moe.opts(gemm_mode=moe.GEMM_DENSE, dense_tile_rows=bm)).y
+        assert_close(y.cpu().numpy(), ref, f"{name} dense tile {bm} with K split")
+    # AUTO with one expert per stage may take either kind: same bits again
+    y = g.forward(moe.opts(pipeline_n=s.EL, exact_order=True)).y
+    assert torch.equal(y, base)
+
+
 @pytest.mark.parametrize("name", ["ragged8", "fine", "one"])
 def test_forward_token_range_stages(name):
     """Token-range stages (each stage all experts over a token range, weights

@@ -74,6 +74,14 @@ def parse_args(argv=None):
     p.add_argument("--gemm-study", action="store_true",
                    help="GroupGemm throughput over group counts, rows per group and CU "
                         "budgets on the DeepSeekV2 expert shape")
+    p.add_argument("--pn-enable", action="store_true",
+                   help="the paper's pipeline enable condition over the zipf loads: eps0 and "
+                        "eps1 per PN, measured (serial stages) and from the library's model")
+    p.add_argument("--side-cus", type=int, default=0,
+                   help="CUs of the CU-masked gather/combine streams (0: no masks)")
+    p.add_argument("--trace-overlap", metavar="CSV", default="",
+                   help="summarise a rocprofv3 kernel-trace CSV of pipelined forwards: when "
+                        "each stage's combine ran against the next stage's GEMMs (no GPU)")
     p.add_argument("--tile-study", action="store_true",
                    help="DenseGemm launch time of one expert for every tile height and "
                         "row count (the data of the launch-cost model)")
@@ -145,7 +153,7 @@ def run_workload(args, shape, inp, steps, warmup, timing=True, serial=False, dev
     chunk = {"experts": moe.CHUNK_EXPERTS, "tokens": moe.CHUNK_TOKENS}[args.chunk_mode]
     o = moe.opts(gemm_mode=mode, pipeline_n=args.pn, gemm_cu_budget=args.cu_budget,
                  dense_min_rows=args.dense_min_rows, timing=timing, chunk_mode=chunk,
-                 serial=serial)
+                 serial=serial, side_cus=args.side_cus)
     g = dev_inputs if dev_inputs is not None else DeviceInputs(inp)
     buf = g.buffers(o)
 
@@ -223,6 +231,8 @@ def main(argv=None):
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
         return 0
+    if args.trace_overlap:
+        return trace_overlap(args.trace_overlap, args.warmup, args.steps)
 
     import torch
 
@@ -241,6 +251,8 @@ def main(argv=None):
         return gemm_study(args)
     if args.tile_study:
         return tile_study(args)
+    if args.pn_enable:
+        return pn_enable(args)
     shape = synth.SHAPES[args.config]
     if args.tokens:
         shape = shape.with_tokens(args.tokens)
@@ -303,7 +315,8 @@ def main(argv=None):
                    "renormalize": shape.renorm, "shared_inter": shape.shared_inter,
                    "gemm_mode": args.mode, "pipeline_n": args.pn,
                    "chunk_mode": args.chunk_mode,
-                   "gemm_cu_budget": args.cu_budget, "parallelism": "single GPU"},
+                   "gemm_cu_budget": args.cu_budget, "side_cus": args.side_cus,
+                   "parallelism": "single GPU"},
         "roofline": {"bound": "hbm" if hbm_bound else "mfma", "achieved": round(achieved, 1),
                      "peak": peak, "unit": "GB/s" if hbm_bound else "TFLOP/s",
                      "frac": round(achieved / peak, 4),
@@ -567,6 +580,101 @@ def gemm_study(args):
                               "dense_ms": round(d_ms, 4), "group_tflops": round(g_tf, 1),
                               "dense_tflops": round(d_tf, 1), "dense_tile_rows": tiles[0]}),
                   flush=True)
+    return 0
+
+
+def pn_enable(args):
+    """Sec. 5.2 item 4 over the zipf loads: for each T and each PN dividing
+    the 20 local experts, eps1 = N G(m/N, E/N) / G(m, E) - 1 (the stages'
+    expert-GEMM time summed, over the unsplit one) and eps0 = N S(m/N) /
+    S(m) - 1 (the same for the combine, the one-GPU stand-in for the
+    all2alls), measured with every stage on one stream (nothing overlapped,
+    every phase timed) and predicted by moe_pipeline_plan from the same row
+    counts; then the PN the library would choose and the pipelined step
+    time at each PN."""
+    import numpy as np
+
+    from paper_2410_12247_amd import moe, synth
+    from paper_2410_12247_amd.workload import DeviceInputs
+
+    base = synth.SHAPES["zipf"]
+    for T in synth.ZIPF_TOKENS:
+        shape = base.with_tokens(T)
+        inp = synth.make_inputs(shape)
+        g = DeviceInputs(inp)
+        meas, model, step = {}, {}, {}
+        counts = None
+        for pn in (1, 2, 4, 5, 10, 20):
+            a = argparse.Namespace(**{**vars(args), "pn": pn, "chunk_mode": "experts"})
+            _, tms, counts = run_workload(a, shape, inp, args.steps, args.warmup, timing=True,
+                                          serial=True, dev_inputs=g)
+            tm = summarize_timing(tms)
+            meas[pn] = (tm["gateup_ms"] + tm["down_ms"], tm["combine_ms"])
+            w, _, _ = run_workload(a, shape, inp, args.steps, args.warmup, timing=False,
+                                   dev_inputs=g)
+            step[pn] = round(w / args.steps * 1e3, 4)
+            model[pn] = moe.pipeline_plan(g.d, moe.opts(), counts, pn)
+        g1, s1 = meas[1]
+        chosen = moe.pipeline_plan(g.d, moe.opts(), counts, 0)["pipeline_n"]
+        print(json.dumps({
+            "pn_enable": "zipf", "tokens": T, "routed_rows": int(np.sum(counts)),
+            "G_ms": round(g1, 4), "S_ms": round(s1, 4),
+            "eps1_measured": {p: round(v[0] / g1 - 1, 4) for p, v in meas.items() if p > 1},
+            "eps0_measured": {p: round(v[1] / s1 - 1, 4) for p, v in meas.items() if p > 1},
+            "eps1_model": {p: round(m["eps1"], 4) for p, m in model.items() if p > 1},
+            "eps0_model": {p: round(m["eps0"], 4) for p, m in model.items() if p > 1},
+            "gain_model_ms": {p: round(m["gain_us"] / 1e3, 4) for p, m in model.items() if p > 1},
+            "enabled_model": {p: m["enabled"] for p, m in model.items() if p > 1},
+            "chosen_pn": chosen, "pipelined_ms": step}), flush=True)
+        del g
+    return 0
+
+
+def trace_overlap(path, warmup, steps):
+    """Stage overlap in a rocprofv3 kernel trace (--kernel-trace, CSV) of a
+    bench.py run with pipelined forwards: each forward starts at a router
+    kernel; the timed forwards are numbers [warmup, warmup + steps) (the
+    benchmark's GEMM-timed steps).  For the combine of each stage the line
+    gives how long it ran, how long of that a GEMM kernel (group_kernel or a
+    K-split fixup, necessarily of a later stage: a stage's combine waits for
+    its own GEMMs) was running too, and whether it started inside such a
+    GEMM's interval.  Prints a markdown table and totals."""
+    import csv
+
+    rows = list(csv.DictReader(open(path)))
+    if not rows:
+        print("empty trace")
+        return 1
+    ev = []
+    for r in rows:
+        name = r.get("Kernel_Name", "")
+        ev.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), name))
+    ev.sort()
+    # forwards start at a router kernel
+    starts = [i for i, e in enumerate(ev) if "route" in e[2] and "select" not in e[2]]
+    fwd = [ev[a:b] for a, b in zip(starts, starts[1:] + [len(ev)])]
+    lines = ["| forward | combine | ran (us) | beside a later GEMM (us) | started inside a "
+             "later GEMM |", "|---|---|---|---|---|"]
+    tot_c, tot_o, n_inside, n_comb = 0.0, 0.0, 0, 0
+    for fi, f in enumerate(fwd[warmup:warmup + steps]):
+        gemms = [e for e in f if "group_kernel" in e[2] or "split_fixup" in e[2]]
+        combs = [e for e in f if "combine_kernel" in e[2]]
+        for ci, (cs, ce, _) in enumerate(combs):
+            # combine i waits for stage i's GEMMs, so any GEMM kernel running
+            # beside it belongs to a later stage
+            ov = 0
+            for gs, ge, _ in gemms:
+                ov += max(0, min(ce, ge) - max(cs, gs))
+            inside = any(gs <= cs < ge for gs, ge, _ in gemms)
+            tot_c += (ce - cs) / 1e3
+            tot_o += ov / 1e3
+            n_inside += int(inside)
+            n_comb += 1
+            lines.append(f"| {fi} | {ci} | {(ce - cs) / 1e3:.1f} | {ov / 1e3:.1f} | "
+                         f"{'yes' if inside else 'no'} |")
+    print("\n".join(lines))
+    print(f"\ncombines: {n_comb}, started inside a GEMM: {n_inside}, "
+          f"combine time {tot_c:.1f} us, of it beside GEMMs {tot_o:.1f} us")
     return 0
 
 

@@ -100,7 +100,9 @@ typedef struct {
                                stage when every expert in it has at least
                                this many rows (Sec. 3.2 Conclusion 1's
                                threshold m), else GroupGemm */
-    int32_t pipeline_n;     /* PN >= 1, the number of pipeline stages */
+    int32_t pipeline_n;     /* PN >= 1, the number of pipeline stages; 0 = chosen
+                               by the library from the row counts (expert
+                               stages only; see moe_pipeline_plan) */
     int32_t gemm_cu_budget; /* workgroups of the persistent grouped GEMM;
                                0 = one per compute unit */
     int32_t flags;          /* MOE_FLAG_TIMING: time each phase with HIP
@@ -127,7 +129,12 @@ typedef struct {
                                expert from its row count (the height whose
                                tile count fills the chip best), or 128, 192,
                                256, 320 to force one */
-    int32_t reserved[1];    /* must be zero */
+    int32_t side_cus;       /* Sec. 5.2's SM control: when the forward uses
+                               its side streams (PN != 1 or shared experts),
+                               0 = no CU masks; > 0 = the gather and combine
+                               streams run on this many CUs (spread over the
+                               XCDs) and the GEMM stream, with its persistent
+                               grid, on the others.  At most 248. */
 } moe_opts;
 
 /* Per-phase device time of the last moe_ffn_forward call on this thread
@@ -138,7 +145,29 @@ typedef struct {
         combine_ms, total_ms;
     int32_t gateup_launches, down_launches; /* GEMM kernel launches timed */
     int32_t dense_stages, group_stages;     /* policy decisions taken */
+    int32_t pipeline_n;                     /* stages the call ran */
 } moe_timing;
+
+/* The paper's pipeline-number analysis (Sec. 5.2 items 4-5) for one
+ * forward, evaluated with the library's cost models. */
+typedef struct {
+    double t_comm_us;   /* T_comm before the split: the combine, one-GPU
+                           stand-in for the dispatch and combine all2alls */
+    double t_comp_us;   /* T_comp before the split: the expert GEMMs */
+    double t_comm_n_us; /* N * S(m/N): the stages' combines, summed */
+    double t_comp_n_us; /* N * G(m/N, E/N): the stages' GEMMs, summed */
+    double eps0;        /* N * S(m/N) / S(m) - 1 */
+    double eps1;        /* N * G(m/N, E/N) / G(m, E) - 1 */
+    double overlap_frac;/* share of the CUs the GEMM grid leaves free for
+                           the side streams (CU budget or side_cus): the
+                           part of L(N) one GPU can realise */
+    double gain_us;     /* L(N) - R(N): min(T_comm, T_comp) (N - 1) / N *
+                           overlap_frac, minus the split's extra GEMM and
+                           combine time and a fixed cost per added stage */
+    int32_t enabled;    /* eps0 <= 0.32 and eps1 <= 0.03 (the values of the
+                           paper's DeepSeekV2 test), or N = 1 */
+    int32_t pipeline_n; /* N */
+} moe_pipeline_eval;
 
 /* Bytes of device workspace: with opts == NULL, what moe_permute needs;
  * with opts != NULL, what moe_ffn_forward needs with those options (a
@@ -289,6 +318,17 @@ moe_status moe_ffn_forward_noalloc(const moe_dims *dims, const moe_opts *opts,
 /* Timing of the last timed moe_ffn_forward on this thread (waits for its
  * events).  Returns MOE_ERR_INVALID when no timed call was made. */
 moe_status moe_last_timing(moe_timing *out);
+
+/* The paper's enable condition and gain for PN = pipeline_n expert stages
+ * (pipeline_n = 0: the PN moe_ffn_forward would choose with pipeline_n = 0,
+ * i.e. the divisor of local_count with the largest positive gain among
+ * those enabled, else 1), from the host row counts rows[0..local_count) of
+ * the local experts.  The GEMM terms use the launch-cost model of the GEMM
+ * kind AUTO (or opts->gemm_mode) takes per stage; the communication terms
+ * the combine's bytes at its measured streaming rate.  Expert stages only.
+ * Host-only; never touches the GPU. */
+moe_status moe_pipeline_plan(const moe_dims *dims, const moe_opts *opts, const int32_t *rows,
+                             int32_t pipeline_n, moe_pipeline_eval *out);
 
 /* The GEMM plan AUTO makes for one pipeline stage (Sec. 3.2 Conclusion 1:
  * GroupGemm and DenseGemm each win over part of the load range; Sec. 4.3:

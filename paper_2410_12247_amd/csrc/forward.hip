@@ -19,6 +19,7 @@
 // expert for large ones).
 #include <algorithm>
 #include <cmath>
+#include <map>
 #include <memory>
 #include <mutex>
 #include <vector>
@@ -49,9 +50,13 @@ enum Phase {
 // host copy of the row counts.  `call` is held for a whole call, so two
 // host threads driving the same device take turns (their enqueues do not
 // interleave on the shared streams, events and pinned buffer).
+struct Streams {
+    hipStream_t sg = nullptr, sm = nullptr, sc = nullptr;
+};
 struct DevState {
     std::mutex call;
-    hipStream_t sg = nullptr, sm = nullptr, sc = nullptr;
+    Streams plain;                     // no CU masks
+    std::map<int, Streams> masked;     // by side_cus: sg, sc on those CUs, sm on the rest
     std::vector<hipEvent_t> sync_ev;   // ordering events (no timing)
     int32_t *pinned_counts = nullptr;  // host-visible copy of counts
     bool ready = false;
@@ -77,14 +82,55 @@ moe_status get_state(DevState **out) {
     if (!g_dev[dev]) g_dev[dev].reset(new DevState);
     DevState &st = *g_dev[dev];
     if (!st.ready) {
-        MOE_HIP(hipStreamCreateWithFlags(&st.sg, hipStreamNonBlocking));
-        MOE_HIP(hipStreamCreateWithFlags(&st.sm, hipStreamNonBlocking));
-        MOE_HIP(hipStreamCreateWithFlags(&st.sc, hipStreamNonBlocking));
+        MOE_HIP(hipStreamCreateWithFlags(&st.plain.sg, hipStreamNonBlocking));
+        MOE_HIP(hipStreamCreateWithFlags(&st.plain.sm, hipStreamNonBlocking));
+        MOE_HIP(hipStreamCreateWithFlags(&st.plain.sc, hipStreamNonBlocking));
         MOE_HIP(hipHostMalloc((void **)&st.pinned_counts, sizeof(int32_t) * kMaxExperts,
                               hipHostMallocDefault));
         st.ready = true;
     }
     *out = &st;
+    return MOE_OK;
+}
+
+// CU masks: the first `side` CUs of the mask for the gather and combine
+// streams, the others for the GEMM stream.  The driver deals a queue's mask
+// bits round-robin over the XCDs and, inside an XCD, over its shader
+// engines, so the first n bits take the same number of CUs from every XCD
+// and engine.  (Measured: a mask that took the side CUs from one engine per
+// XCD left that engine half of its CUs for an equal share of the GEMM's
+// workgroups and doubled the GEMM time.)
+void side_cu_masks(int side, int cus, std::vector<uint32_t> &side_mask,
+                   std::vector<uint32_t> &gemm_mask) {
+    const int words = (cus + 31) / 32;
+    side_mask.assign(words, 0u);
+    gemm_mask.assign(words, 0u);
+    for (int c = 0; c < cus; ++c) {
+        if (c < side) side_mask[c / 32] |= 1u << (c % 32);
+        else gemm_mask[c / 32] |= 1u << (c % 32);
+    }
+}
+
+// Streams of a call: the plain ones, or (side > 0) the set whose gather and
+// combine streams run on `side` CUs and whose GEMM stream runs on the rest
+// (created once per device and side count, default priority).
+moe_status get_streams(DevState *st, int side, Streams *out) {
+    if (side <= 0) {
+        *out = st->plain;
+        return MOE_OK;
+    }
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto it = st->masked.find(side);
+    if (it == st->masked.end()) {
+        std::vector<uint32_t> sm_mask, gm_mask;
+        side_cu_masks(side, device_cu_count(), sm_mask, gm_mask);
+        Streams s;
+        MOE_HIP(hipExtStreamCreateWithCUMask(&s.sg, (uint32_t)sm_mask.size(), sm_mask.data()));
+        MOE_HIP(hipExtStreamCreateWithCUMask(&s.sc, (uint32_t)sm_mask.size(), sm_mask.data()));
+        MOE_HIP(hipExtStreamCreateWithCUMask(&s.sm, (uint32_t)gm_mask.size(), gm_mask.data()));
+        it = st->masked.emplace(side, s).first;
+    }
+    *out = it->second;
     return MOE_OK;
 }
 
@@ -96,6 +142,7 @@ struct TimedSpan {
 struct TimingRecord {
     std::vector<TimedSpan> spans;
     int gateup_launches = 0, down_launches = 0, dense_stages = 0, group_stages = 0;
+    int pipeline_n = 0;
     bool valid = false;
 };
 thread_local TimingRecord g_timing;
@@ -165,8 +212,11 @@ moe_status check_opts(const moe_dims *d, const moe_opts *o) {
     if (o->dense_min_rows < 0) return fail(MOE_ERR_INVALID, "dense_min_rows < 0");
     if (o->chunk_mode != MOE_CHUNK_EXPERTS && o->chunk_mode != MOE_CHUNK_TOKENS)
         return fail(MOE_ERR_INVALID, "chunk_mode %d unknown", o->chunk_mode);
-    if (o->pipeline_n < 1) return fail(MOE_ERR_INVALID, "pipeline_n %d < 1", o->pipeline_n);
-    if (o->chunk_mode == MOE_CHUNK_EXPERTS && d->local_count % o->pipeline_n)
+    if (o->pipeline_n < 0) return fail(MOE_ERR_INVALID, "pipeline_n %d < 0", o->pipeline_n);
+    if (o->pipeline_n == 0 && o->chunk_mode != MOE_CHUNK_EXPERTS)
+        return fail(MOE_ERR_INVALID, "pipeline_n 0 (chosen by the library) needs expert stages");
+    if (o->chunk_mode == MOE_CHUNK_EXPERTS && o->pipeline_n > 0 &&
+        d->local_count % o->pipeline_n)
         return fail(MOE_ERR_INVALID, "pipeline_n %d must divide local_count %d",
                     o->pipeline_n, d->local_count);
     if (o->chunk_mode == MOE_CHUNK_TOKENS &&
@@ -180,7 +230,8 @@ moe_status check_opts(const moe_dims *d, const moe_opts *o) {
     if (o->dense_tile_rows != 0 && !valid_tile_rows(o->dense_tile_rows))
         return fail(MOE_ERR_INVALID, "dense_tile_rows %d is not 0, 128, 192, 256 or 320",
                     o->dense_tile_rows);
-    if (o->reserved[0]) return fail(MOE_ERR_INVALID, "reserved options must be zero");
+    if (o->side_cus < 0 || o->side_cus > kMaxExperts - 8)
+        return fail(MOE_ERR_INVALID, "side_cus %d outside [0, 248]", o->side_cus);
     return MOE_OK;
 }
 
@@ -193,7 +244,8 @@ int forward_buckets(const moe_dims *d, const moe_opts *o) {
 
 // Experts per pipeline stage.
 int stage_experts(const moe_dims &d, const moe_opts &o) {
-    return o.chunk_mode == MOE_CHUNK_TOKENS ? d.local_count : d.local_count / o.pipeline_n;
+    if (o.chunk_mode == MOE_CHUNK_TOKENS) return d.local_count;
+    return o.pipeline_n > 0 ? d.local_count / o.pipeline_n : 1;
 }
 
 bool needs_host_counts(const moe_dims &d, const moe_opts &o) {
@@ -201,7 +253,7 @@ bool needs_host_counts(const moe_dims &d, const moe_opts &o) {
     // stage gathers, and for AUTO to weigh the two GEMM kinds: with a fixed
     // threshold only when some expert can reach it (an expert has at most T
     // rows), with the cost model only for stages of few experts
-    if (o.gemm_mode == MOE_GEMM_DENSE || o.pipeline_n > 1) return true;
+    if (o.gemm_mode == MOE_GEMM_DENSE || o.pipeline_n != 1) return true;
     if (o.gemm_mode != MOE_GEMM_AUTO) return false;
     if (o.dense_min_rows > 0) return o.dense_min_rows <= d.tokens;
     return stage_experts(d, o) <= kAutoDenseMaxExperts;
@@ -235,6 +287,102 @@ bool auto_picks_dense(const moe_dims &d, const moe_opts &o, const int32_t *rows,
     if (o.dense_min_rows > 0) return min_rows >= o.dense_min_rows;
     if (n > kAutoDenseMaxExperts) return false;
     return dus < gus;
+}
+
+// ---- pipeline-number model (Sec. 5.2 items 4-5) ---------------------------
+// On one GPU the communication of a stage is the stand-in for its two
+// all2alls: the stage's combine (its gather is folded into the GEMM).  Its
+// time comes from its bytes at the combine's measured streaming rate; the
+// GEMM time of a stage from the launch-cost model of the GEMM kind AUTO
+// would take for it.
+constexpr double kCombineBytesPerUs = 5.6e6;  // ~5.6 TB/s, combine_kernel on MI355X
+constexpr double kCombineLaunchUs = 4.0;
+// Fixed cost of one more stage: the event hops between the GEMM and
+// combine streams and the launches they separate.
+constexpr double kStageUs = 20.0;
+// The paper's thresholds for its DeepSeekV2 test (Sec. 5.2 item 4).
+constexpr double kEps0Max = 0.32, kEps1Max = 0.03;
+
+// A combine reads its stage's rows and every token's slot records; it
+// writes every token's output when it starts y, and otherwise reads and
+// writes only the tokens with a row in the stage (at most min(T, rows)).
+double combine_us(const moe_dims &d, int64_t rows, bool accumulate) {
+    const double touched = (double)std::min<int64_t>(d.tokens, rows);
+    const double bytes = (double)rows * d.hidden * 4 +
+                         (accumulate ? touched * d.hidden * 8 : (double)d.tokens * d.hidden * 4) +
+                         (double)d.tokens * d.top_k * 8;
+    return kCombineLaunchUs + bytes / kCombineBytesPerUs;
+}
+
+// GEMM and combine time of the expert stages of pipeline number n over the
+// host row counts rows[0..EL).
+void stage_times(const moe_dims &d, const moe_opts &o, const int32_t *rows, int n, int grid,
+                 bool split, double *comm_us, double *comp_us) {
+    const int EL = d.local_count, per = EL / n;
+    double comm = 0.0, comp = 0.0;
+    for (int i = 0; i < n; ++i) {
+        const int32_t *r = rows + i * per;
+        double gus = 0.0, dus = 0.0;
+        const bool pick = auto_picks_dense(d, o, r, per, grid, split, &gus, &dus);
+        const bool dense = o.gemm_mode == MOE_GEMM_DENSE || (o.gemm_mode == MOE_GEMM_AUTO && pick);
+        comp += dense ? dus : gus;
+        int64_t stage_rows = 0;
+        for (int e = 0; e < per; ++e) stage_rows += r[e];
+        comm += combine_us(d, stage_rows, d.shared_inter > 0 || i > 0);
+    }
+    *comm_us = comm;
+    *comp_us = comp;
+}
+
+// The paper's terms for pipeline number n: T_comm and T_comp before the
+// split, their sums over n stages (n S(m/n) and n G(m/n, E/n)), the
+// enable-condition ratios and the gain L(n) - R(n).  The paper's
+// L(n) = min(T_comm, T_comp) (n - 1) / n assumes the communication kernels
+// run on SMs of their own beside the GEMM; on one GPU the persistent GEMM
+// grid holds every CU it is given, so only the CUs it leaves free (a CU
+// budget or side CUs) can run a combine beside it, and L is scaled by that
+// fraction (none by default: measured, a combine next to a full-grid GEMM
+// only runs in its tail).  R(n) is the overhead of cutting: the extra GEMM
+// and combine time of n stages plus a fixed cost per added stage.
+moe_pipeline_eval pipeline_eval(const moe_dims &d, const moe_opts &o, const int32_t *rows, int n,
+                                int grid, bool split) {
+    moe_pipeline_eval ev{};
+    stage_times(d, o, rows, 1, grid, split, &ev.t_comm_us, &ev.t_comp_us);
+    stage_times(d, o, rows, n, grid, split, &ev.t_comm_n_us, &ev.t_comp_n_us);
+    ev.eps0 = ev.t_comm_us > 0 ? ev.t_comm_n_us / ev.t_comm_us - 1.0 : 0.0;
+    ev.eps1 = ev.t_comp_us > 0 ? ev.t_comp_n_us / ev.t_comp_us - 1.0 : 0.0;
+    const int cus = device_cu_count();
+    ev.overlap_frac = cus > grid ? (double)(cus - grid) / cus : 0.0;
+    const double C = std::min(ev.t_comm_us, ev.t_comp_us);
+    const double R = (ev.t_comp_n_us - ev.t_comp_us) + (ev.t_comm_n_us - ev.t_comm_us) +
+                     (n - 1) * kStageUs;
+    ev.gain_us = n > 1 ? C * (n - 1) / n * ev.overlap_frac - R : 0.0;
+    ev.enabled = (n == 1 || (ev.eps0 <= kEps0Max && ev.eps1 <= kEps1Max)) ? 1 : 0;
+    return ev;
+}
+
+// pipeline_n = 0: the divisor of EL with the largest positive predicted gain
+// among those that meet the enable condition, else 1.
+int choose_pipeline_auto(const moe_dims &d, const moe_opts &o, const int32_t *rows, int grid,
+                         bool split) {
+    int best = 1;
+    double best_gain = 0.0;
+    for (int n = 2; n <= d.local_count; ++n) {
+        if (d.local_count % n) continue;
+        const moe_pipeline_eval ev = pipeline_eval(d, o, rows, n, grid, split);
+        if (ev.enabled && ev.gain_us > best_gain) {
+            best = n;
+            best_gain = ev.gain_us;
+        }
+    }
+    return best;
+}
+
+int gemm_grid(const moe_opts &o) {
+    int cus = device_cu_count();
+    int grid = o.gemm_cu_budget > 0 ? o.gemm_cu_budget : cus;
+    if (o.side_cus > 0) grid = std::min(grid, cus - o.side_cus);
+    return std::max(8, (grid / 8) * 8);
 }
 
 // Scratch of the no-allocation entry point: one static buffer per device
@@ -303,9 +451,9 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
     float *y_perm = reinterpret_cast<float *>(base + L.y_perm);
     bf16_t *shared_act = reinterpret_cast<bf16_t *>(base + L.shared_act);
 
-    const int PN = o->pipeline_n;
+    // pipeline number: given, or (0) chosen from the row counts below
+    int PN = o->pipeline_n;
     const int EL = d.local_count;
-    const int per_stage = tok_stages ? EL : EL / PN;  // buckets per stage
     const int64_t tps = tok_stages ? (d.tokens + PN - 1) / PN : 0;
     // One stage without shared experts has nothing to overlap: every step
     // runs on the caller's stream (no cross-stream event hops, which cost
@@ -313,18 +461,23 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
     // may overlap, and the no-allocation entry point (no internal streams).
     // Otherwise gather, GEMMs and combine run on their own streams so that
     // stages (and the shared FFN) overlap.
+    // (A library-chosen PN counts as pipelined here: the streams are set up
+    // before the row counts are known.)
     const bool one_stream =
         st == nullptr || (PN == 1 && !has_shared) || (o->flags & MOE_FLAG_SERIAL) != 0;
+    const int max_pn = PN > 0 ? PN : EL;
     hipEvent_t ev_fork = nullptr, ev_counts = nullptr, ev_done = nullptr, ev_start = nullptr;
     hipEvent_t *ev_g = nullptr, *ev_m = nullptr;
+    Streams strm;
     if (st) {
-        MOE_TRY(ensure_events(st->sync_ev, 3 * (size_t)PN + 4, hipEventDisableTiming));
+        MOE_TRY(ensure_events(st->sync_ev, 3 * (size_t)max_pn + 4, hipEventDisableTiming));
         ev_fork = st->sync_ev[0];
         ev_counts = st->sync_ev[1];
         ev_done = st->sync_ev[2];
         ev_start = st->sync_ev[3];
         ev_g = &st->sync_ev[4];
-        ev_m = ev_g + PN;
+        ev_m = ev_g + max_pn;
+        if (!one_stream) MOE_TRY(get_streams(st, o->side_cus, &strm));
     }
 
     const bool timing = st && (o->flags & (MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM)) != 0;
@@ -337,9 +490,9 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         tpool = &t_time_ev[dev];
     }
     Timer tm(tpool, timing ? o->flags : 0);
-    hipStream_t sg = one_stream ? s0 : st->sg;
-    hipStream_t sm = one_stream ? s0 : st->sm;
-    hipStream_t sc = one_stream ? s0 : st->sc;
+    hipStream_t sg = one_stream ? s0 : strm.sg;
+    hipStream_t sm = one_stream ? s0 : strm.sm;
+    hipStream_t sc = one_stream ? s0 : strm.sc;
     const int H = d.hidden, I = d.inter;
     const int64_t T = d.tokens;
 
@@ -351,10 +504,10 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         MOE_HIP(hipStreamWaitEvent(sm, ev_start, 0));
         tm.gap();
     }
-    // persistent grid of the grouped GEMMs and their K-split scratch (all
-    // on the GEMM stream, one GEMM after another)
-    int grid = o->gemm_cu_budget > 0 ? o->gemm_cu_budget : device_cu_count();
-    grid = std::max(8, (grid / 8) * 8);
+    // persistent grid of the grouped GEMMs (at most the CUs the GEMM stream
+    // may use) and their K-split scratch (all on the GEMM stream, one GEMM
+    // after another)
+    const int grid = gemm_grid(*o);
     const bool split = (o->flags & MOE_FLAG_EXACT_ORDER) == 0;
     float *split_part = split ? reinterpret_cast<float *>(base + L.split_part) : nullptr;
     int32_t *split_meta = split ? reinterpret_cast<int32_t *>(base + L.split_meta) : nullptr;
@@ -400,6 +553,13 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         tm.gap();
         hc.assign(st->pinned_counts, st->pinned_counts + NB);
     }
+    if (PN == 0) {
+        PN = choose_pipeline_auto(d, *o, hc.data(), grid, split);
+        if (timing) g_timing.pipeline_n = PN;
+    } else if (timing) {
+        g_timing.pipeline_n = PN;
+    }
+    const int per_stage = tok_stages ? EL : EL / PN;  // buckets per stage
     // the grouped gate/up GEMM can gather its token rows itself while every
     // byte offset into x fits 32 bits
     const bool fold_ok = gather_foldable(d);
@@ -521,6 +681,31 @@ using namespace moe;
 
 extern "C" {
 
+moe_status moe_pipeline_plan(const moe_dims *dims, const moe_opts *opts, const int32_t *rows,
+                             int32_t pipeline_n, moe_pipeline_eval *out) {
+    MOE_TRY(check_dims(dims));
+    moe_opts defaults{};
+    defaults.pipeline_n = 1;
+    const moe_opts *o = opts ? opts : &defaults;
+    MOE_TRY(check_opts(dims, o));
+    if (o->chunk_mode != MOE_CHUNK_EXPERTS)
+        return fail(MOE_ERR_INVALID, "moe_pipeline_plan: expert stages only");
+    if (!rows || !out) return fail(MOE_ERR_INVALID, "moe_pipeline_plan: NULL rows or out");
+    const int EL = dims->local_count;
+    for (int e = 0; e < EL; ++e)
+        if (rows[e] < 0) return fail(MOE_ERR_INVALID, "moe_pipeline_plan: rows[%d] < 0", e);
+    const int grid = gemm_grid(*o);
+    const bool split = (o->flags & MOE_FLAG_EXACT_ORDER) == 0;
+    int n = pipeline_n;
+    if (n == 0) n = choose_pipeline_auto(*dims, *o, rows, grid, split);
+    if (n < 1 || EL % n)
+        return fail(MOE_ERR_INVALID, "moe_pipeline_plan: pipeline_n %d must divide %d",
+                    pipeline_n, EL);
+    *out = pipeline_eval(*dims, *o, rows, n, grid, split);
+    out->pipeline_n = n;
+    return MOE_OK;
+}
+
 moe_status moe_gemm_plan(const moe_dims *dims, const moe_opts *opts, int32_t n_experts,
                          const int32_t *rows, int32_t *dense, int32_t *tile_rows,
                          double *group_us, double *dense_us) {
@@ -535,8 +720,7 @@ moe_status moe_gemm_plan(const moe_dims *dims, const moe_opts *opts, int32_t n_e
     if (!rows || !dense) return fail(MOE_ERR_INVALID, "moe_gemm_plan: NULL rows or dense");
     for (int e = 0; e < n_experts; ++e)
         if (rows[e] < 0) return fail(MOE_ERR_INVALID, "moe_gemm_plan: rows[%d] < 0", e);
-    int grid = o->gemm_cu_budget > 0 ? o->gemm_cu_budget : device_cu_count();
-    grid = std::max(8, (grid / 8) * 8);
+    const int grid = gemm_grid(*o);
     const bool split = (o->flags & MOE_FLAG_EXACT_ORDER) == 0;
     bool d_ = auto_picks_dense(*dims, *o, rows, n_experts, grid, split, group_us, dense_us);
     if (o->gemm_mode == MOE_GEMM_GROUP) d_ = false;
@@ -668,6 +852,7 @@ moe_status moe_last_timing(moe_timing *out) {
     out->down_launches = g_timing.down_launches;
     out->dense_stages = g_timing.dense_stages;
     out->group_stages = g_timing.group_stages;
+    out->pipeline_n = g_timing.pipeline_n;
     return MOE_OK;
 }
 

@@ -24,7 +24,7 @@ FLAG_TIMING, FLAG_TIMING_GEMM, FLAG_EXACT_ORDER, FLAG_SERIAL = 1, 2, 4, 8
 EXPORTS = ("moe_workspace_bytes", "moe_route", "moe_permute", "moe_gather", "moe_ffn_group",
            "moe_ffn_dense", "moe_combine", "moe_ffn_forward", "moe_ffn_forward_noalloc",
            "moe_last_timing",
-           "moe_gemm_plan", "moe_choose_pipeline_n", "moe_status_string",
+           "moe_gemm_plan", "moe_pipeline_plan", "moe_choose_pipeline_n", "moe_status_string",
            "moe_last_error")
 
 
@@ -46,14 +46,24 @@ class Opts(ctypes.Structure):
     _fields_ = [("gemm_mode", ctypes.c_int32), ("dense_min_rows", ctypes.c_int32),
                 ("pipeline_n", ctypes.c_int32), ("gemm_cu_budget", ctypes.c_int32),
                 ("flags", ctypes.c_int32), ("chunk_mode", ctypes.c_int32),
-                ("dense_tile_rows", ctypes.c_int32), ("reserved", ctypes.c_int32 * 1)]
+                ("dense_tile_rows", ctypes.c_int32), ("side_cus", ctypes.c_int32)]
 
 
 class Timing(ctypes.Structure):
     _fields_ = [(n, ctypes.c_float) for n in ("route_ms", "permute_ms", "gather_ms", "gateup_ms",
                                              "down_ms", "shared_ms", "combine_ms", "total_ms")] + \
                [(n, ctypes.c_int32) for n in ("gateup_launches", "down_launches",
-                                             "dense_stages", "group_stages")]
+                                             "dense_stages", "group_stages", "pipeline_n")]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+class PipelineEval(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("t_comm_us", "t_comp_us", "t_comm_n_us",
+                                              "t_comp_n_us", "eps0", "eps1", "overlap_frac",
+                                              "gain_us")] + \
+               [("enabled", ctypes.c_int32), ("pipeline_n", ctypes.c_int32)]
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}
@@ -82,6 +92,7 @@ def lib():
     L.moe_ffn_forward.argtypes = [D, O, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
     L.moe_ffn_forward_noalloc.argtypes = [D, O, P, P, P, P, P, P, P, P, P, P, P, P, P, P]
     L.moe_last_timing.argtypes = [ctypes.POINTER(Timing)]
+    L.moe_pipeline_plan.argtypes = [D, O, P, I32, ctypes.POINTER(PipelineEval)]
     L.moe_gemm_plan.argtypes = [D, O, I32, P, ctypes.POINTER(I32), P,
                                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     L.moe_choose_pipeline_n.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double, I32,
@@ -91,7 +102,7 @@ def lib():
     L.moe_last_error.restype = ctypes.c_char_p
     for name in ("moe_route", "moe_permute", "moe_gather", "moe_ffn_group", "moe_ffn_dense",
                  "moe_combine", "moe_ffn_forward", "moe_ffn_forward_noalloc", "moe_last_timing",
-                 "moe_choose_pipeline_n", "moe_gemm_plan"):
+                 "moe_choose_pipeline_n", "moe_gemm_plan", "moe_pipeline_plan"):
         getattr(L, name).restype = I32
     _lib = L
     return L
@@ -113,7 +124,7 @@ def dims(tokens, hidden, inter, experts, top_k, local_begin=0, local_count=None,
 
 def opts(gemm_mode=GEMM_AUTO, dense_min_rows=0, pipeline_n=1, gemm_cu_budget=0,
          timing=False, chunk_mode=CHUNK_EXPERTS, exact_order=False, serial=False,
-         dense_tile_rows=0) -> Opts:
+         dense_tile_rows=0, side_cus=0) -> Opts:
     """timing: False, True (every phase) or "gemm" (the GEMM launches only).
     exact_order: no K split of the grouped GEMM's last round (the same bits
     for every pipeline number, stage kind, CU budget and GEMM kind).
@@ -128,6 +139,7 @@ def opts(gemm_mode=GEMM_AUTO, dense_min_rows=0, pipeline_n=1, gemm_cu_budget=0,
         o.flags |= FLAG_SERIAL
     o.chunk_mode = chunk_mode
     o.dense_tile_rows = dense_tile_rows
+    o.side_cus = side_cus
     return o
 
 
@@ -214,6 +226,18 @@ def last_timing() -> dict:
     t = Timing()
     _check(lib().moe_last_timing(ctypes.byref(t)))
     return t.as_dict()
+
+
+def pipeline_plan(d: Dims, o: Optional[Opts], rows, pipeline_n: int) -> dict:
+    """The paper's pipeline terms for PN = pipeline_n (0: the library's
+    choice) from host row counts per local expert."""
+    import numpy as np
+    r = np.ascontiguousarray(rows, dtype=np.int32)
+    ev = PipelineEval()
+    _check(lib().moe_pipeline_plan(ctypes.byref(d), ctypes.byref(o) if o is not None else None,
+                                   r.ctypes.data_as(ctypes.c_void_p), int(pipeline_n),
+                                   ctypes.byref(ev)))
+    return ev.as_dict()
 
 
 def gemm_plan(d: Dims, o: Optional[Opts], rows):

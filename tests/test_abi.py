@@ -81,8 +81,9 @@ def test_invalid_options_and_buffers_rejected():
     L = moe.lib()
     d = moe.dims(64, 256, 128, 8, 2)
     fake = ctypes.c_void_p(16)
-    for o in (moe.opts(pipeline_n=3), moe.opts(pipeline_n=0), moe.opts(gemm_mode=7),
-              moe.opts(gemm_cu_budget=-1)):
+    for o in (moe.opts(pipeline_n=3), moe.opts(pipeline_n=-1), moe.opts(gemm_mode=7),
+              moe.opts(gemm_cu_budget=-1), moe.opts(side_cus=-1),
+              moe.opts(pipeline_n=0, chunk_mode=moe.CHUNK_TOKENS)):
         st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake,
                                fake, None, None, None, fake, None, None, None, fake, 1 << 40,
                                None)
@@ -111,8 +112,7 @@ def test_invalid_options_and_buffers_rejected():
     assert moe.opts(timing="gemm").flags == 2 and moe.opts(timing=True).flags == 1
     assert moe.opts(exact_order=True).flags == 4
     assert moe.opts(timing="gemm", exact_order=True).flags == 6
-    o = moe.opts()
-    o.reserved[0] = 5
+    o = moe.opts(side_cus=250)  # at most 248 CUs for the side streams
     st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake, fake,
                            None, None, None, fake, None, None, None, fake, 1 << 40, None)
     assert st == 1
@@ -271,3 +271,70 @@ def test_gemm_plan_model():
                            None) == 1
     assert L.moe_gemm_plan(ctypes.byref(d), None, 1, None, ctypes.byref(out), None, None,
                            None) == 1
+
+
+def test_pipeline_enable_condition():
+    """moe_pipeline_plan evaluates the paper's enable condition (Sec. 5.2
+    item 4: N S(m/N) / S(m) <= 1 + eps0 and N G(m/N, E/N) / G(m, E) <=
+    1 + eps1, eps0 = 0.32 and eps1 = 0.03 as in its DeepSeekV2 test) and
+    gain L(N) - R(N) (item 5); pipeline_n = 0 picks the enabled divisor
+    with the largest positive gain.  Checked against the definitions on
+    the terms the call reports."""
+    plan = moe.pipeline_plan
+    d = moe.dims(16384, 5120, 1536, 160, 6, 0, 20, False)
+    rows = [600 + 37 * e for e in range(20)]
+    one = plan(d, moe.opts(), rows, 1)
+    assert one["eps0"] == 0 and one["eps1"] == 0 and one["gain_us"] == 0 and one["enabled"]
+    assert one["t_comm_us"] == one["t_comm_n_us"] and one["t_comp_us"] == one["t_comp_n_us"]
+    for n in (2, 4, 5, 10, 20):
+        ev = plan(d, moe.opts(), rows, n)
+        assert ev["pipeline_n"] == n
+        assert ev["t_comm_us"] == one["t_comm_us"] and ev["t_comp_us"] == one["t_comp_us"]
+        assert ev["eps0"] == pytest.approx(ev["t_comm_n_us"] / ev["t_comm_us"] - 1)
+        assert ev["eps1"] == pytest.approx(ev["t_comp_n_us"] / ev["t_comp_us"] - 1)
+        C = min(ev["t_comm_us"], ev["t_comp_us"])
+        R = (ev["t_comp_n_us"] - ev["t_comp_us"]) + (ev["t_comm_n_us"] - ev["t_comm_us"])
+        assert ev["overlap_frac"] == 0.0   # the full grid leaves no CU to the combine
+        assert C * (n - 1) / n * ev["overlap_frac"] - R - ev["gain_us"] == \
+            pytest.approx(20.0 * (n - 1))
+        # a CU budget of 192 of 256 leaves a quarter of the CUs to the side streams
+        eb = plan(d, moe.opts(gemm_cu_budget=192), rows, n)
+        assert eb["overlap_frac"] == 0.25
+        Cb = min(eb["t_comm_us"], eb["t_comp_us"])
+        Rb = (eb["t_comp_n_us"] - eb["t_comp_us"]) + (eb["t_comm_n_us"] - eb["t_comm_us"])
+        assert Cb * (n - 1) / n * 0.25 - Rb - eb["gain_us"] == pytest.approx(20.0 * (n - 1))
+        assert plan(d, moe.opts(side_cus=64), rows, n)["overlap_frac"] == 0.25
+        assert ev["enabled"] == int(ev["eps0"] <= 0.32 and ev["eps1"] <= 0.03)
+        # cutting never makes the stages' work smaller than the whole
+        assert ev["eps0"] > 0 and ev["eps1"] > -1e-9
+    # the library's choice: the best enabled divisor, else 1
+    best = plan(d, moe.opts(), rows, 0)
+    cands = [plan(d, moe.opts(), rows, n) for n in (2, 4, 5, 10, 20)]
+    ok = [c for c in cands if c["enabled"] and c["gain_us"] > 0]
+    assert best["pipeline_n"] == (max(ok, key=lambda c: c["gain_us"])["pipeline_n"] if ok else 1)
+    # one GPU: each stage's combine re-reads and re-writes all of y, so the
+    # stand-in communication does not split (eps0 far above 0.32) and no PN
+    # is enabled on the Mixtral- or DeepSeekV2-shaped loads
+    mix = moe.dims(16384, 4096, 3584, 8, 2)
+    assert plan(mix, moe.opts(), [4096] * 8, 2)["eps0"] > 0.32
+    assert plan(mix, moe.opts(), [4096] * 8, 0)["pipeline_n"] == 1
+    assert plan(d, moe.opts(), rows, 0)["pipeline_n"] == 1
+    # PN must divide the local experts; expert stages only
+    with pytest.raises(moe.MoEError):
+        plan(d, moe.opts(), rows, 3)
+    with pytest.raises(moe.MoEError):
+        plan(d, moe.opts(chunk_mode=moe.CHUNK_TOKENS, pipeline_n=2), rows, 2)
+    with pytest.raises(moe.MoEError):
+        plan(d, moe.opts(), [-1] + rows[1:], 2)
+
+
+def test_binding_structs_match_the_header():
+    """The ctypes mirrors of moe_opts, moe_timing and moe_pipeline_eval have
+    the header's sizes and field order (a mismatch would shift every field
+    after it), and convert to dicts."""
+    assert ctypes.sizeof(moe.Opts) == 8 * 4
+    assert ctypes.sizeof(moe.Timing) == 8 * 4 + 5 * 4
+    assert ctypes.sizeof(moe.PipelineEval) == 8 * 8 + 2 * 4
+    assert [f for f, _ in moe.Opts._fields_][-2:] == ["dense_tile_rows", "side_cus"]
+    assert moe.Timing().as_dict()["pipeline_n"] == 0
+    assert set(moe.PipelineEval().as_dict()) >= {"eps0", "eps1", "gain_us", "enabled"}

@@ -272,6 +272,32 @@ def test_forward_invariant_to_pipeline_and_gemm_kind(name):
 
 
 @pytest.mark.parametrize("name", ["ragged8", "fine"])
+def test_side_cus_and_library_pipeline_number(name):
+    """CU-masked side streams (the gather and combine streams on side_cus
+    CUs, the GEMM stream and its grid on the rest) and the library's own
+    choice of PN (pipeline_n = 0, after the row counts): same bits as the
+    unmasked forward in exact order, and the chosen PN is the one
+    moe_pipeline_plan gives for those counts."""
+    inp, ids, w = case(name)
+    g = Dev(inp)
+    s = inp.shape
+    base = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP, exact_order=True)).y.clone()
+    for side in (8, 32, 64):
+        for pn in [p for p in (1, 2, 4) if s.EL % p == 0]:
+            y = g.forward(moe.opts(pipeline_n=pn, side_cus=side, exact_order=True)).y
+            assert torch.equal(y, base), f"side_cus={side} PN={pn} changes the bits"
+    buf = g.forward(moe.opts(pipeline_n=0, timing=True, exact_order=True))
+    assert torch.equal(buf.y, base)
+    chosen = moe.last_timing()["pipeline_n"]
+    counts = buf.counts.cpu().numpy()
+    plan = moe.pipeline_plan(g.d, moe.opts(pipeline_n=0, exact_order=True), counts, 0)
+    assert chosen == plan["pipeline_n"]
+    ref = oracle_y(inp, ids, w, np.arange(s.T))
+    y = g.forward(moe.opts(pipeline_n=0, side_cus=32)).y
+    assert_close(y.cpu().numpy(), ref, f"{name} PN auto, side CUs")
+
+
+@pytest.mark.parametrize("name", ["ragged8", "fine"])
 def test_forward_timing_modes(name):
     """Timing every phase or only the GEMMs leaves the result unchanged; the
     GEMM-only mode reports GEMM time and zero for the other phases, on one

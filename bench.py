@@ -82,6 +82,10 @@ def parse_args(argv=None):
     p.add_argument("--trace-overlap", metavar="CSV", default="",
                    help="summarise a rocprofv3 kernel-trace CSV of pipelined forwards: when "
                         "each stage's combine ran against the next stage's GEMMs (no GPU)")
+    p.add_argument("--trace-stats", metavar="CSV", default="",
+                   help="per-kernel durations from a rocprofv3 kernel-trace CSV of a bench.py "
+                        "run, over its timed forwards only (--warmup, --steps as in that "
+                        "run; no GPU)")
     p.add_argument("--tile-study", action="store_true",
                    help="DenseGemm launch time of one expert for every tile height and "
                         "row count (the data of the launch-cost model)")
@@ -126,8 +130,20 @@ def cpu_baseline(inp, target_s):
         n = int(min(s.T, max(n, n * target_s / max(dt, 1e-3))))
         dt = run(n)
     return {"value": n / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": f"{n} of {s.T} tokens of the same workload (routing + MoE FFN output "
                       f"per token, fp64 expert rows), {dt:.1f} s wall"}
+
+
+def cpu_model():
+    """The host CPU's model name (first 'model name' line of /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def copy_calibration(nbytes):
@@ -157,21 +173,18 @@ def run_workload(args, shape, inp, steps, warmup, timing=True, serial=False, dev
     g = dev_inputs if dev_inputs is not None else DeviceInputs(inp)
     buf = g.buffers(o)
 
-    def step():
-        g.run(buf)
-        return moe.last_timing() if timing else None
-
     for _ in range(warmup):
-        step()
+        g.run(buf)
     torch.cuda.synchronize()
-    tms = []
+    if timing and warmup > 0:
+        moe.last_timing()  # the record of the warm-up calls is dropped
     t0 = time.perf_counter()
     for _ in range(steps):
-        tm = step()
-        if tm:
-            tms.append(tm)
+        g.run(buf)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    # timed calls add up in the library until read: one read after the loop
+    tms = [moe.last_timing()] if timing else []
     counts = buf.counts.cpu().numpy()
     return wall, tms, counts
 
@@ -217,8 +230,13 @@ def phase_bytes(s, R, accumulate):
 
 
 def summarize_timing(tms):
-    keys = tms[0].keys()
-    return {k: sum(t[k] for t in tms) / len(tms) for k in keys}
+    """Per-call averages of moe_last_timing records (each may sum several
+    timed calls)."""
+    calls = sum(t["calls"] for t in tms)
+    out = {k: sum(t[k] for t in tms) / calls for k in tms[0].keys()}
+    out["pipeline_n"] = tms[-1]["pipeline_n"]
+    out["calls"] = calls
+    return out
 
 
 def main(argv=None):
@@ -233,6 +251,8 @@ def main(argv=None):
         return 0
     if args.trace_overlap:
         return trace_overlap(args.trace_overlap, args.warmup, args.steps)
+    if args.trace_stats:
+        return trace_stats(args.trace_stats, args.warmup, args.steps)
 
     import torch
 
@@ -630,6 +650,71 @@ def pn_enable(args):
     return 0
 
 
+def _kernel_label(name):
+    """Short kernel name: the function and its first template argument."""
+    base = name[5:] if name.startswith("void ") else name
+    base = base.replace("moe::(anonymous namespace)::", "").replace("moe::", "").split("(")[0]
+    if "<" in base:
+        head, rest = base.split("<", 1)
+        first = rest.split(",")[0].split(">")[0].strip()
+        tile = ""
+        if "PingPong<" in rest:
+            tile = " BM=" + rest.split("PingPong<", 1)[1].split(">")[0].split(",")[-1].strip()
+        return f"{head}<{first}>{tile}"
+    return base
+
+
+def _trace_forwards(path):
+    """Kernel dispatches of a kernel-trace CSV, cut into forwards: each starts
+    at the shared-expert offsets kernel when the workload has shared experts,
+    else at the router."""
+    import csv
+
+    ev = []
+    for r in csv.DictReader(open(path)):
+        ev.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]),
+                   _kernel_label(r.get("Kernel_Name", ""))))
+    ev.sort()
+    has_shared = any("shared_offsets" in e[2] for e in ev)
+    first = (lambda n: "shared_offsets" in n) if has_shared else \
+        (lambda n: n.startswith("route") and "select" not in n)
+    starts = [i for i, e in enumerate(ev) if first(e[2])]
+    fwd = [ev[a:b] for a, b in zip(starts, starts[1:] + [len(ev)])]
+    return fwd, has_shared
+
+
+def trace_stats(path, warmup, steps):
+    """Average duration of each kernel over the timed forwards [warmup,
+    warmup + steps) of a kernel trace of one bench.py run (the GEMM-timed
+    steps whose HIP events give the line's roofline), and over every
+    forward in the trace for comparison.  With shared experts the first
+    grouped gate/up and down launches of a forward are the shared FFN's."""
+    fwd, has_shared = _trace_forwards(path)
+
+    def stats(forwards):
+        acc = {}
+        for f in forwards:
+            seen = {}
+            for s_, e_, n in f:
+                k = n
+                if has_shared and n.startswith("group_kernel"):
+                    seen[n] = seen.get(n, 0) + 1
+                    k = n + (" (shared)" if seen[n] == 1 else " (routed)")
+                acc.setdefault(k, []).append((e_ - s_) / 1e3)
+        return acc
+
+    timed = stats(fwd[warmup:warmup + steps])
+    every = stats(fwd)
+    print(f"forwards in trace: {len(fwd)}; timed: [{warmup}, {warmup + steps})\n")
+    print("| kernel | calls (timed) | avg us (timed) | min | max | calls (all) | avg us (all) |")
+    print("|---|---|---|---|---|---|---|")
+    for k in sorted(timed, key=lambda k: -sum(timed[k])):
+        t, a = timed[k], every[k]
+        print(f"| {k} | {len(t)} | {sum(t) / len(t):.1f} | {min(t):.1f} | {max(t):.1f} | "
+              f"{len(a)} | {sum(a) / len(a):.1f} |")
+    return 0
+
+
 def trace_overlap(path, warmup, steps):
     """Stage overlap in a rocprofv3 kernel trace (--kernel-trace, CSV) of a
     bench.py run with pipelined forwards: each forward starts at a router
@@ -639,20 +724,7 @@ def trace_overlap(path, warmup, steps):
     K-split fixup, necessarily of a later stage: a stage's combine waits for
     its own GEMMs) was running too, and whether it started inside such a
     GEMM's interval.  Prints a markdown table and totals."""
-    import csv
-
-    rows = list(csv.DictReader(open(path)))
-    if not rows:
-        print("empty trace")
-        return 1
-    ev = []
-    for r in rows:
-        name = r.get("Kernel_Name", "")
-        ev.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), name))
-    ev.sort()
-    # forwards start at a router kernel
-    starts = [i for i, e in enumerate(ev) if "route" in e[2] and "select" not in e[2]]
-    fwd = [ev[a:b] for a, b in zip(starts, starts[1:] + [len(ev)])]
+    fwd, _ = _trace_forwards(path)
     lines = ["| forward | combine | ran (us) | beside a later GEMM (us) | started inside a "
              "later GEMM |", "|---|---|---|---|---|"]
     tot_c, tot_o, n_inside, n_comb = 0.0, 0.0, 0, 0

@@ -137,15 +137,19 @@ typedef struct {
                                grid, on the others.  At most 248. */
 } moe_opts;
 
-/* Per-phase device time of the last moe_ffn_forward call on this thread
- * that had MOE_FLAG_TIMING or MOE_FLAG_TIMING_GEMM set, in milliseconds,
- * summed over stages. */
+/* Per-phase device time, in milliseconds summed over stages and over the
+ * timed moe_ffn_forward calls (MOE_FLAG_TIMING or MOE_FLAG_TIMING_GEMM) this
+ * thread made on one device since it last called moe_last_timing (`calls`
+ * of them), so a timed loop needs one read at its end, not a host sync per
+ * step.  Launch and stage counts add up the same way; pipeline_n is the
+ * last call's. */
 typedef struct {
     float route_ms, permute_ms, gather_ms, gateup_ms, down_ms, shared_ms,
         combine_ms, total_ms;
     int32_t gateup_launches, down_launches; /* GEMM kernel launches timed */
     int32_t dense_stages, group_stages;     /* policy decisions taken */
-    int32_t pipeline_n;                     /* stages the call ran */
+    int32_t pipeline_n;                     /* stages the last call ran */
+    int32_t calls;                          /* timed calls summed */
 } moe_timing;
 
 /* The paper's pipeline-number analysis (Sec. 5.2 items 4-5) for one
@@ -281,7 +285,7 @@ moe_status moe_combine(const moe_dims *dims, int32_t e_first, int32_t e_count,
  * Thread safety: calls from several host threads on one device are
  * serialised inside the library (the side streams, ordering events and the
  * pinned copy of the counts are per device); moe_last_timing reads the
- * calling thread's own last timed call. */
+ * calling thread's own timed calls. */
 moe_status moe_ffn_forward(const moe_dims *dims, const moe_opts *opts, const moe_bf16 *x,
                            const float *w_router, const float *bias,
                            const moe_bf16 *w_gate, const moe_bf16 *w_up,
@@ -315,8 +319,9 @@ moe_status moe_ffn_forward_noalloc(const moe_dims *dims, const moe_opts *opts,
                                    float *y, int32_t *topk_ids, float *topk_w, int32_t *counts,
                                    void *stream);
 
-/* Timing of the last timed moe_ffn_forward on this thread (waits for its
- * events).  Returns MOE_ERR_INVALID when no timed call was made. */
+/* Timing of the timed moe_ffn_forward calls on this thread since the
+ * previous read (waits for their events); the next timed call then starts a
+ * new record.  Returns MOE_ERR_INVALID when no timed call was made. */
 moe_status moe_last_timing(moe_timing *out);
 
 /* The paper's enable condition and gain for PN = pipeline_n expert stages

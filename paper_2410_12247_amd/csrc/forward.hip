@@ -143,7 +143,11 @@ struct TimingRecord {
     std::vector<TimedSpan> spans;
     int gateup_launches = 0, down_launches = 0, dense_stages = 0, group_stages = 0;
     int pipeline_n = 0;
+    int calls = 0;       // timed calls in the record
+    int device = -1;     // device of the record's events
+    size_t events = 0;   // events of the pool in use by the record
     bool valid = false;
+    bool read = false;   // returned by moe_last_timing: the next timed call starts anew
 };
 thread_local TimingRecord g_timing;
 // timing events of the calling thread, per device: a thread's last timed
@@ -158,7 +162,9 @@ class Timer {
    public:
     Timer(std::vector<hipEvent_t> *pool, int flags)
         : pool_(pool), all_((flags & MOE_FLAG_TIMING) != 0),
-          gemm_((flags & (MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM)) != 0) {}
+          gemm_((flags & (MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM)) != 0),
+          used_(g_timing.events) {}
+    ~Timer() { g_timing.events = used_; }
     // Starts a span of `phase` on stream s; returns its index (or -1).
     moe_status begin(hipStream_t s, int phase, int *idx = nullptr) {
         int &i = idx ? *idx : cur_;
@@ -199,7 +205,7 @@ class Timer {
     }
     std::vector<hipEvent_t> *pool_;
     bool all_, gemm_;
-    size_t used_ = 0;
+    size_t used_;
     int cur_ = -1;
     bool chain_ = false;  // the last enqueue was a span's stop event
     hipStream_t last_s_ = nullptr;
@@ -483,11 +489,17 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
     const bool timing = st && (o->flags & (MOE_FLAG_TIMING | MOE_FLAG_TIMING_GEMM)) != 0;
     std::vector<hipEvent_t> *tpool = nullptr;
     if (timing) {
-        g_timing = TimingRecord{};
+        // a record that was read, or that holds another device's events,
+        // starts anew; otherwise this call's spans are added to it
         int dev = 0;
         MOE_HIP(hipGetDevice(&dev));
         if ((int)t_time_ev.size() <= dev) t_time_ev.resize(dev + 1);
         tpool = &t_time_ev[dev];
+        if (g_timing.read || g_timing.device != dev) {
+            g_timing = TimingRecord{};
+            g_timing.device = dev;
+        }
+        ++g_timing.calls;
     }
     Timer tm(tpool, timing ? o->flags : 0);
     hipStream_t sg = one_stream ? s0 : strm.sg;
@@ -853,6 +865,8 @@ moe_status moe_last_timing(moe_timing *out) {
     out->dense_stages = g_timing.dense_stages;
     out->group_stages = g_timing.group_stages;
     out->pipeline_n = g_timing.pipeline_n;
+    out->calls = g_timing.calls;
+    g_timing.read = true;
     return MOE_OK;
 }
 

@@ -53,7 +53,8 @@ class Timing(ctypes.Structure):
     _fields_ = [(n, ctypes.c_float) for n in ("route_ms", "permute_ms", "gather_ms", "gateup_ms",
                                              "down_ms", "shared_ms", "combine_ms", "total_ms")] + \
                [(n, ctypes.c_int32) for n in ("gateup_launches", "down_launches",
-                                             "dense_stages", "group_stages", "pipeline_n")]
+                                             "dense_stages", "group_stages", "pipeline_n",
+                                             "calls")]
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}

@@ -333,7 +333,7 @@ def test_binding_structs_match_the_header():
     the header's sizes and field order (a mismatch would shift every field
     after it), and convert to dicts."""
     assert ctypes.sizeof(moe.Opts) == 8 * 4
-    assert ctypes.sizeof(moe.Timing) == 8 * 4 + 5 * 4
+    assert ctypes.sizeof(moe.Timing) == 8 * 4 + 6 * 4
     assert ctypes.sizeof(moe.PipelineEval) == 8 * 8 + 2 * 4
     assert [f for f, _ in moe.Opts._fields_][-2:] == ["dense_tile_rows", "side_cus"]
     assert moe.Timing().as_dict()["pipeline_n"] == 0

@@ -318,6 +318,14 @@ def test_forward_timing_modes(name):
         assert t_gemm["gateup_launches"] == t_all["gateup_launches"] >= 1
         if inp.shape.n_shared:
             assert t_gemm["shared_ms"] > 0
+        # timed calls add up until read: three calls, one read
+        for _ in range(3):
+            y = g.forward(moe.opts(pipeline_n=pn, timing="gemm")).y
+        t3 = moe.last_timing()
+        assert t3["calls"] == 3 and t_gemm["calls"] == 1
+        assert t3["gateup_launches"] == 3 * t_gemm["gateup_launches"]
+        assert t3["group_stages"] == 3 * t_gemm["group_stages"]
+        assert torch.equal(y, base)
 
 
 @pytest.mark.parametrize("name", ["tall4", "ragged8", "window"])
@@ -464,3 +472,42 @@ def test_zero_tokens_is_a_noop():
                 None, y, None, None, None, ws)
     torch.cuda.synchronize()
     assert torch.all(y == 3.0)
+
+
+def test_forward_from_two_host_threads():
+    """Two host threads calling moe_ffn_forward on one device at once, each on
+    its own torch stream and buffers, with options that use the library's
+    side streams, events and pinned counts (shared experts, PN = 2, DenseGemm
+    needing host row counts): every result has the bits of the same call made
+    alone."""
+    import threading
+
+    names = ("fine", "ragged8")
+    opts = {"fine": moe.opts(pipeline_n=2, exact_order=True),
+            "ragged8": moe.opts(gemm_mode=moe.GEMM_DENSE, pipeline_n=4, exact_order=True)}
+    devs = {n: Dev(case(n)[0]) for n in names}
+    ref = {n: devs[n].forward(opts[n]).y.clone() for n in names}
+    errors = []
+
+    def worker(n):
+        try:
+            g = devs[n]
+            s = torch.cuda.Stream()
+            buf = g.buffers(opts[n])
+            with torch.cuda.stream(s):
+                for _ in range(20):
+                    g.run(buf, stream=s)
+                    s.synchronize()
+                    if not torch.equal(buf.y, ref[n]):
+                        errors.append(f"{n}: bits differ")
+                        return
+        except Exception as e:  # reported below
+            errors.append(f"{n}: {e!r}")
+
+    threads = [threading.Thread(target=worker, args=(n,)) for n in names]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads), "a forward thread did not finish"
+    assert not errors, errors

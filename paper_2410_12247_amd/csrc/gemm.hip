@@ -109,8 +109,15 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
     return (uint32_t)ua | ((uint32_t)ub << 16);
 }
 
+// silu(g) * u = g * u / (1 + e^-g), with the hardware's exp2 and
+// reciprocal (about 1 ulp each; the result is rounded to bf16 next):
+// e^-g = 2^(-g log2 e).  An IEEE-rounded reciprocal costs a ten-instruction
+// division sequence per value, and the gate/up epilogue evaluates 80 of
+// them per lane with every wave of the workgroup in its epilogue at once.
+// Large |g| behaves: e^-g -> inf gives 0 (silu -> 0), e^-g -> 0 gives g.
 __device__ __forceinline__ float silu_mul(float g, float u) {
-    return g * __frcp_rn(1.0f + __expf(-g)) * u;
+    const float e = __builtin_amdgcn_exp2f(g * -1.44269504088896341f);
+    return g * __builtin_amdgcn_rcpf(1.0f + e) * u;
 }
 
 // One output tile.  Global -> LDS copies are wave-wide LDS-DMA loads

@@ -14,6 +14,10 @@
 // rounded to fp32 once; the full-softmax denominator is a DPP wave sum.
 #include "common.h"
 
+#include <type_traits>
+
+#include "route_lane_asm.h"
+
 namespace moe {
 namespace {
 
@@ -164,17 +168,17 @@ __device__ __forceinline__ void dma16_to_lds(const void *gptr, uint32_t lds_addr
                  : "memory");
 }
 
+// Register-tiled router for more than 16 experts.
+//
 // Logits phase layout: 256 threads = TG token groups x EG expert groups
-// (EG = 16, or 8 when E <= 8 so that no thread repeats an expert); a thread
+// (EG = 16, or 32 for 129 to 160 experts); a thread
 // owns TT tokens (tg + TG i: consecutive lanes read rows 36 floats apart, so
 // eight lanes of a 16-byte LDS read land on distinct banks) x TE experts
 // (TE = ceil(E / EG)) and keeps their fma chains in registers.  x and the
 // router are staged through two LDS buffers HC h at a time: the router rows
 // by LDS-DMA, x through registers (widened to fp32), the next chunk in
 // flight while the current one is multiplied; per 4 h a thread reads
-// TT + TE float4 and issues 4*TT*TE fmas.  With few experts the fmas per
-// chunk are few, so the chunk is longer (HC = 128) to keep more bytes in
-// flight per wait.
+// TT + TE float4 and issues 4*TT*TE fmas.
 //
 // TT tokens per thread, so a workgroup routes TG*TT <= 64 tokens; the
 // launcher picks TT so that the grid keeps several workgroups per compute
@@ -491,38 +495,314 @@ __global__ __launch_bounds__(RT_THREADS) void route_select_kernel(const float *_
     select_token(z + t * E, t, E, k, renorm, threadIdx.x & 63, ids, wout);
 }
 
+// Lane-per-token router for E <= 16.  Lane l of a wave owns the chains of
+// token l % TPW for R * G experts (the wave's 64 lanes are R sets of TPW =
+// 64 / R tokens; set s takes G experts of its own): x is the lane's own
+// operand, and the router element of each fma comes from a register that
+// holds 16 consecutive h in each 16-lane row, broadcast by DPP (see
+// route_lane_asm.h), so a stage of 64 h costs 64 G fmas plus 64 bf16
+// widenings per lane and no LDS traffic per fma.  Each chain is still one
+// fp32 fma per h in ascending order from +0, bias added at the end.
+//
+// A workgroup is NW compute waves (64 / R tokens x NW * R * G experts, all of
+// E) and one producer wave.  Per stage the producer stages the x rows
+// (16-byte chunk c of row r at place c ^ lane_swz(r), so the 16-byte reads
+// of 8 or 16 consecutive rows fall on distinct banks) and every router row's
+// 64 h into an LDS ring of NS stages by LDS-DMA, NS - 1 to NS stages ahead,
+// waits for the next stage and meets the compute waves at a barrier; the
+// compute waves only read LDS and run the fmas (a stage's operands are read
+// during the previous stage's fmas).  Issuing the DMA from the compute waves
+// themselves left it behind their VALU stream: measured on the Mixtral shape
+// (16384 tokens, H = 4096, 8 experts), 41 us that way against 36 us with the
+// producer wave.  The logits then go to LDS and one lane per token takes the
+// top-k and the softmax weights.
+constexpr int RL_HS = 64;     // h per stage
+constexpr int RL_NS_MAX = 6;  // ring stages at most (deeper rings measured no faster)
+
+// Ring depth for stages of `stage` bytes and `per` DMA requests per stage:
+// even (register sets alternate with the slots), at most 80 KiB (two
+// workgroups per compute unit) and with (depth - 1) * per requests countable
+// by the 6-bit vmcnt.
+constexpr int lane_ring(int stage, int per) {
+    int n = RL_NS_MAX;
+    while (n > 2 && (n * stage > 80 * 1024 || (n - 1) * per > 63)) n -= 2;
+    return n;
+}
+
+// Calls f(integral_constant<int, I>) for I = B .. N - 1.
+template <int B, int N, class F>
+__device__ __forceinline__ void lane_unroll(F &&f) {
+    if constexpr (B < N) {
+        f(std::integral_constant<int, B>{});
+        lane_unroll<B + 1, N>(f);
+    }
+}
+
+template <int G>
+struct LaneRegs {
+    u32x4 x[8];     // the lane's 64 bf16 of the stage
+    floatx4 w[G];   // router rows: w[g][c] = w[e_g][h0 + 4 (lane % 16) + c]
+};
+
+// this lane's first operands, read and waited for
+template <int G>
+__device__ __forceinline__ void lane_read(LaneRegs<G> &r, const uint32_t (&ax)[8], uint32_t aw) {
+    if constexpr (G == 2) {
+        asm volatile(
+            "ds_read_b128 %0, %10\n\tds_read_b128 %1, %11\n\tds_read_b128 %2, %12\n\t"
+            "ds_read_b128 %3, %13\n\tds_read_b128 %4, %14\n\tds_read_b128 %5, %15\n\t"
+            "ds_read_b128 %6, %16\n\tds_read_b128 %7, %17\n\t"
+            "ds_read_b128 %8, %18\n\tds_read_b128 %9, %18 offset:256\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(r.x[0]), "=&v"(r.x[1]), "=&v"(r.x[2]), "=&v"(r.x[3]), "=&v"(r.x[4]),
+              "=&v"(r.x[5]), "=&v"(r.x[6]), "=&v"(r.x[7]), "=&v"(r.w[0]), "=&v"(r.w[1])
+            : "v"(ax[0]), "v"(ax[1]), "v"(ax[2]), "v"(ax[3]), "v"(ax[4]), "v"(ax[5]),
+              "v"(ax[6]), "v"(ax[7]), "v"(aw)
+            : "memory");
+    } else {
+        static_assert(G == 4, "two or four experts per lane");
+        asm volatile(
+            "ds_read_b128 %0, %12\n\tds_read_b128 %1, %13\n\tds_read_b128 %2, %14\n\t"
+            "ds_read_b128 %3, %15\n\tds_read_b128 %4, %16\n\tds_read_b128 %5, %17\n\t"
+            "ds_read_b128 %6, %18\n\tds_read_b128 %7, %19\n\t"
+            "ds_read_b128 %8, %20\n\tds_read_b128 %9, %20 offset:256\n\t"
+            "ds_read_b128 %10, %20 offset:512\n\tds_read_b128 %11, %20 offset:768\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(r.x[0]), "=&v"(r.x[1]), "=&v"(r.x[2]), "=&v"(r.x[3]), "=&v"(r.x[4]),
+              "=&v"(r.x[5]), "=&v"(r.x[6]), "=&v"(r.x[7]), "=&v"(r.w[0]), "=&v"(r.w[1]),
+              "=&v"(r.w[2]), "=&v"(r.w[3])
+            : "v"(ax[0]), "v"(ax[1]), "v"(ax[2]), "v"(ax[3]), "v"(ax[4]), "v"(ax[5]),
+              "v"(ax[6]), "v"(ax[7]), "v"(aw)
+            : "memory");
+    }
+}
+
+// one stage's fmas from cur, the next stage's operands (LDS byte offset OFF
+// from the addresses ax / aw) read into nxt
+template <int G, int OFF>
+__device__ __forceinline__ void lane_stage(float (&acc)[G], const LaneRegs<G> &cur,
+                                           LaneRegs<G> &nxt, const uint32_t (&ax)[8],
+                                           uint32_t aw) {
+    if constexpr (G == 2)
+        lane_stage_g2<OFF, OFF>(acc, cur.x, cur.w, nxt.x, nxt.w, ax, aw);
+    else
+        lane_stage_g4<OFF, OFF>(acc, cur.x, cur.w, nxt.x, nxt.w, ax, aw);
+}
+
+// Place of a row's chunks in the x stage: 128-byte rows sit in one half of
+// the 256 bytes the 64 banks span (row parity), so rows r and r + 2 share
+// banks unless their places differ; r ^ (r >> 3) gives distinct places to
+// any 8 consecutive rows and to the 8 rows of each parity among 16
+// consecutive ones.
+__device__ __forceinline__ int lane_swz(int r) { return (r ^ (r >> 3)) & 7; }
+
+// s_waitcnt vmcnt(PER * n) for n == K, K - 1, .., 0
+template <int PER, int K>
+__device__ __forceinline__ void lane_wait_vm_k(int n) {
+    if (n == K) {
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(K * PER) : "memory");
+    } else if constexpr (K > 0) {
+        lane_wait_vm_k<PER, K - 1>(n);
+    }
+}
+
+// s_waitcnt vmcnt(PER * n), 0 <= n <= NS - 1; n == NS - 2 at every stage
+// but the first and the last few
+template <int PER, int NS>
+__device__ __forceinline__ void lane_wait_vm(int n) {
+    static_assert((NS - 1) * PER <= 63, "vmcnt range");
+    if (__builtin_expect(n == NS - 2, 1)) {
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 2) * PER) : "memory");
+        return;
+    }
+    lane_wait_vm_k<PER, NS - 1>(n);
+}
+
+// top-k and softmax weights of one token from its E logits, by one lane
+template <int EP>
+__device__ __forceinline__ void select_lane(const float *zrow, int64_t t, int E, int k,
+                                            int renorm, int32_t *__restrict__ ids,
+                                            float *__restrict__ wout) {
+    uint64_t key[EP];
+    float z[EP];
+#pragma unroll
+    for (int e = 0; e < EP; ++e) {
+        z[e] = e < E ? zrow[e] : 0.0f;
+        key[e] = e < E ? logit_key(z[e], e) : 0ull;
+    }
+    int sel_e[kMaxTopK];
+    float sel_z[kMaxTopK];
+#pragma unroll
+    for (int j = 0; j < kMaxTopK; ++j) {
+        sel_e[j] = 0;
+        sel_z[j] = 0.0f;
+        if (j < k) {
+            uint64_t best = key[0];
+#pragma unroll
+            for (int e = 1; e < EP; ++e) best = max_u64(best, key[e]);
+            sel_e[j] = (int)(0xFFFFFFFFu - (uint32_t)best);
+            sel_z[j] = key_logit(best);
+#pragma unroll
+            for (int e = 0; e < EP; ++e)
+                if (key[e] == best) key[e] = 0ull;
+        }
+    }
+    const double zmax = (double)sel_z[0];
+    double denom = 0.0;
+    if (renorm) {
+#pragma unroll
+        for (int j = 0; j < kMaxTopK; ++j)
+            if (j < k) denom += exp((double)sel_z[j] - zmax);
+    } else {
+#pragma unroll
+        for (int e = 0; e < EP; ++e)
+            if (e < E) denom += exp((double)z[e] - zmax);
+    }
+#pragma unroll
+    for (int j = 0; j < kMaxTopK; ++j) {
+        if (j < k) {
+            ids[t * k + j] = sel_e[j];
+            wout[t * k + j] = (float)(exp((double)sel_z[j] - zmax) / denom);
+        }
+    }
+}
+
+template <int G, int R, int NW, int NS>
+__global__ __launch_bounds__(64 * NW + 64) void route_lane_kernel(const bf16_t *__restrict__ x,
+                                                             const float *__restrict__ wr,
+                                                             const float *__restrict__ bias,
+                                                             int64_t T, int H, int E, int k,
+                                                             int renorm,
+                                                             int32_t *__restrict__ ids,
+                                                             float *__restrict__ wout) {
+    constexpr int TPW = 64 / R;              // tokens per wave (and per workgroup)
+    constexpr int EP = NW * R * G;           // experts per workgroup (>= E)
+    constexpr int XB = TPW * RL_HS * 2;      // bytes of a stage's x rows
+    constexpr int WB = EP * RL_HS * 4;       // bytes of a stage's router rows
+    constexpr int STAGE = XB + WB;
+    constexpr int NXR = XB / 1024;           // wave-wide 16-byte DMA requests
+    constexpr int NWR = WB / 1024;
+    constexpr int PER = NXR + NWR;           // requests per stage (producer wave)
+    static_assert(XB % 1024 == 0 && WB % 1024 == 0, "stages of whole requests");
+    static_assert(NS % 2 == 0 && NS >= 2 && NS * STAGE <= 160 * 1024, "ring depth");
+    static_assert(TPW * (EP + 1) * 4 <= NS * STAGE, "logits fit in the ring");
+    // ring slots reached from one base address through the 16-bit offset of
+    // ds_read; the slots past them use a second base
+    constexpr int SPB = 65535 / STAGE + 1 < NS ? 65535 / STAGE + 1 : NS;
+    static_assert(2 * SPB >= NS, "two base addresses cover the ring");
+    __shared__ __attribute__((aligned(16))) char lds[NS * STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const bool producer = wave == NW;
+    const int tl = lane % TPW;                   // token of this lane
+    const int eb = (wave * R + lane / TPW) * G;  // its first expert (compute waves)
+    const int64_t t0 = (int64_t)blockIdx.x * TPW;
+
+    // the producer's DMA requests q of a stage: q < NXR: 8 x rows of 128
+    // bytes (lane i: row 8 q + i / 8, 16-byte chunk (i % 8) ^ lane_swz(row)
+    // into place i % 8); else 4 router rows of 256 bytes
+    const char *src[PER];
+    uint32_t dst[PER];
+    int step_bytes[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        if (q < NXR) {
+            const int r = q * 8 + (lane >> 3);
+            const int c = (lane & 7) ^ lane_swz(r);
+            const int64_t t = min<int64_t>(t0 + r, T - 1);
+            src[q] = reinterpret_cast<const char *>(x + t * H) + c * 16;
+            dst[q] = q * 1024;
+            step_bytes[q] = RL_HS * 2;
+        } else {
+            const int qw = q - NXR;
+            const int e = min(qw * 4 + (lane >> 4), E - 1);  // rows past E: a copy, never used
+            src[q] = reinterpret_cast<const char *>(wr + (int64_t)e * H) + (lane & 15) * 16;
+            dst[q] = XB + qw * 1024;
+            step_bytes[q] = RL_HS * 4;
+        }
+    }
+    auto issue = [&](int st) {  // stage st into ring slot st % NS
+        char *slot = lds + (st % NS) * STAGE;
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+            __builtin_amdgcn_global_load_lds((gbl_void_t *)(src[j] + (int64_t)st * step_bytes[j]),
+                                             (lds_void_t *)(slot + dst[j]), 16, 0, 0);
+    };
+
+    // LDS byte addresses in ring slot 0 (set 0) and slot SPB (set 1): chunk c
+    // of this lane's x row, and its router chunk (lane % 16) of expert eb
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void_t *)lds;
+    uint32_t ax[2][8], aw[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+            ax[b][c] = lds0 + b * SPB * STAGE + tl * (RL_HS * 2) + ((c ^ lane_swz(tl)) << 4);
+        aw[b] = lds0 + b * SPB * STAGE + XB + eb * (RL_HS * 4) + (lane & 15) * 16;
+    }
+
+    const int nst = H / RL_HS;
+    const int pre = min(NS, nst);
+    float acc[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g] = 0.0f;
+    if (producer) {
+        // stages 0 .. NS - 1 in flight; before each barrier the next stage
+        // has landed, after it the slot of the stage the compute waves have
+        // just taken into registers is refilled
+        for (int st = 0; st < pre; ++st) issue(st);
+        lane_wait_vm<PER, NS>(pre - 1);  // stage 0
+        __builtin_amdgcn_s_barrier();
+        for (int st = 0; st + 1 < nst; ++st) {
+            lane_wait_vm<PER, NS>(min(NS - 2, nst - 2 - st));  // stage st + 1
+            __builtin_amdgcn_s_barrier();
+            if (st + NS < nst) issue(st + NS);
+        }
+    } else {
+        __builtin_amdgcn_s_barrier();  // stage 0 landed
+        LaneRegs<G> regs[2];
+        lane_read<G>(regs[0], ax[0], aw[0]);
+        // stage st: its operands are in regs[st % 2]; at the barrier stage
+        // st + 1 has landed and slot st % NS (read in step st - 1) is free
+        auto step = [&](int st, auto slot_c) {
+            constexpr int U = decltype(slot_c)::value;  // st % NS
+            constexpr int NXT = (U + 1) % NS;           // slot read for stage st + 1
+            constexpr int B = NXT >= SPB;
+            if (st >= nst) return;
+            if (st + 1 < nst) __builtin_amdgcn_s_barrier();
+            // (after the last stage the reads of the next slot return unused data)
+            lane_stage<G, (NXT - B * SPB) * STAGE>(acc, regs[U & 1], regs[(U + 1) & 1],
+                                                   ax[B], aw[B]);
+        };
+        for (int st0 = 0; st0 < nst; st0 += NS)
+            lane_unroll<0, NS>([&](auto u) { step(st0 + decltype(u)::value, u); });
+    }
+    __syncthreads();  // no wave reads the ring any more; no DMA in flight
+
+    // logits to LDS, zs[token][e] with an odd row stride
+    float *zs = reinterpret_cast<float *>(lds);
+    constexpr int ZLD = EP + 1;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        const int e = eb + g;
+        if (e < E && !producer) zs[tl * ZLD + e] = bias ? acc[g] + bias[e] : acc[g];
+    }
+    __syncthreads();
+    if (wave == 0 && lane < TPW) {
+        const int64_t t = t0 + lane;
+        if (t < T) select_lane<EP>(zs + lane * ZLD, t, E, k, renorm, ids, wout);
+    }
+}
+
 template <int TE, int TT, int EG>
 hipError_t launch_tt(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                      int32_t *ids, float *w, hipStream_t s) {
     constexpr int TOK = RT_THREADS / EG * TT;
     const int64_t blocks = (d.tokens + TOK - 1) / TOK;
-    // longer chunks when few experts give little work per chunk (H is a
-    // multiple of 64; 128-h chunks need a multiple of 128).  256-h chunks
-    // wait half as often; they are taken when two workgroups still fit a
-    // CU's 160 KiB of LDS, or when the grid does not fill the chip anyway
-    // (measured: DBRX T = 8192 0.117 -> 0.105 ms, Mixtral T = 64 0.062 ->
-    // 0.053 ms; at Mixtral T = 16384 one workgroup per CU, 0.095 -> 0.131 ms)
-    if constexpr (TE == 1) {
-        constexpr size_t lds256 = (2 * (size_t)TOK * (256 + 4) + 2 * (size_t)EG * 256) * 4;
-        constexpr bool fits = lds256 <= 160 * 1024;
-        constexpr bool two_fit = 2 * lds256 <= 160 * 1024;
-        if constexpr (fits) {
-            if (d.hidden % 256 == 0 && (two_fit || blocks <= device_cu_count())) {
-                route_kernel<TE, TT, EG, 256><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
-                    x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
-                return hipGetLastError();
-            }
-        }
-        if (d.hidden % 128 == 0)
-            route_kernel<TE, TT, EG, 128><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
-                x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
-        else
-            route_kernel<TE, TT, EG, 64><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
-                x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
-    } else {
-        route_kernel<TE, TT, EG, 32><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
-            x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
-    }
+    route_kernel<TE, TT, EG, 32><<<(unsigned)blocks, RT_THREADS, 0, s>>>(
+        x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
     return hipGetLastError();
 }
 
@@ -537,6 +817,41 @@ hipError_t launch_te(const moe_dims &d, const bf16_t *x, const float *wr, const 
         return launch_tt<TE, (TG * 4 <= 64 ? 4 : 1), EG>(d, x, wr, bias, ids, w, s);
     if (d.tokens >= (int64_t)TG * 2 * 2 * cus) return launch_tt<TE, 2, EG>(d, x, wr, bias, ids, w, s);
     return launch_tt<TE, 1, EG>(d, x, wr, bias, ids, w, s);
+}
+
+template <int G, int R, int NW>
+hipError_t launch_lane(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
+                       int32_t *ids, float *w, hipStream_t s) {
+    constexpr int TPW = 64 / R;
+    constexpr int STAGE = TPW * RL_HS * 2 + NW * R * G * RL_HS * 4;
+    constexpr int PER = STAGE / 1024;
+    const int64_t blocks = (d.tokens + TPW - 1) / TPW;
+    route_lane_kernel<G, R, NW, lane_ring(STAGE, PER)><<<(unsigned)blocks, 64 * NW + 64, 0, s>>>(
+        x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
+    return hipGetLastError();
+}
+
+// Per-SIMD fma work of a lane-router shape: every wave issues (G + 1) VALU
+// instructions per h (G fmas and one widening); waves beyond one per SIMD
+// queue behind each other.
+double lane_cost(int64_t tokens, int tpw, int waves_per_block, int g) {
+    const double waves = (double)((tokens + tpw - 1) / tpw) * waves_per_block;
+    const double simds = 4.0 * device_cu_count();
+    return (waves > simds ? waves / simds : 1.0) * (g + 1);
+}
+
+// Two experts per lane (the most waves, each with the fewest instructions
+// per h) up to 8 experts at every batch size measured (64 to 65536 tokens);
+// 9 to 16 experts take four per lane once the batch fills every SIMD with
+// two-expert waves (measured, E = 16, H = 6144: 8192 tokens 51 us with two
+// against 73 us with four, 16384 tokens 85 against 76 us).
+hipError_t launch_lane_router(const moe_dims &d, const bf16_t *x, const float *wr,
+                              const float *bias, int32_t *ids, float *w, hipStream_t s) {
+    if (d.experts <= 4) return launch_lane<2, 1, 2>(d, x, wr, bias, ids, w, s);
+    if (d.experts <= 8) return launch_lane<2, 1, 4>(d, x, wr, bias, ids, w, s);
+    if (lane_cost(d.tokens, 64, 4, 4) < lane_cost(d.tokens, 32, 4, 2))
+        return launch_lane<4, 1, 4>(d, x, wr, bias, ids, w, s);
+    return launch_lane<2, 2, 4>(d, x, wr, bias, ids, w, s);
 }
 
 }  // namespace
@@ -558,13 +873,12 @@ hipError_t launch_stream(const moe_dims &d, const bf16_t *x, const float *wr, co
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                         int32_t *ids, float *w, float *logits, hipStream_t s) {
     if (d.tokens <= 0) return hipSuccess;
-    if (d.experts <= 8) return launch_te<1, 8>(d, x, wr, bias, ids, w, s);
+    if (d.experts <= 16) return launch_lane_router(d, x, wr, bias, ids, w, s);
     // many experts, few tokens: the register-tiled kernel has too few
     // workgroups to cover its serial h loop, so the streaming kernel spreads
     // expert blocks over more workgroups (logits through the caller's
-    // buffer, then the selection kernel).  With E <= 16 the register-tiled
-    // kernel is faster at every T measured (1 to 16384 tokens).
-    if (d.experts > 16 && logits && d.tokens <= kRouteStreamMaxTokens)
+    // buffer, then the selection kernel)
+    if (logits && d.tokens <= kRouteStreamMaxTokens)
         return launch_stream<16>(d, x, wr, bias, ids, w, logits, s);
     // 129..160 experts below 65536 tokens: 32 expert groups of 5, with the
     // most tokens per thread that keeps ~2 waves per SIMD (T / 4096, at most
@@ -578,7 +892,6 @@ hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, con
         return launch_tt<5, 1, 32>(d, x, wr, bias, ids, w, s);
     }
     const int te = (d.experts + 15) / 16;
-    if (te <= 1) return launch_te<1>(d, x, wr, bias, ids, w, s);
     if (te <= 2) return launch_te<2>(d, x, wr, bias, ids, w, s);
     if (te <= 4) return launch_te<4>(d, x, wr, bias, ids, w, s);
     if (te <= 8) return launch_te<8>(d, x, wr, bias, ids, w, s);

@@ -134,6 +134,35 @@ def test_maximum_experts_and_top_k(T, E, k):
     assert_close(buf.y.cpu().numpy(), oracle_y(inp, ids, w, np.arange(T)), f"E={E} k={k}")
 
 
+@pytest.mark.parametrize("T,E,H,k,renorm,use_bias", [
+    (1, 1, 64, 1, True, False),         # one token, one expert, one stage
+    (100, 3, 128, 2, False, True),      # E <= 4: two waves of 2 experts, two stages
+    (60000, 4, 64, 2, True, False),     # E <= 4, a large batch
+    (1000, 5, 448, 2, True, True),      # 7 stages: not a multiple of the 6-slot ring
+    (16383, 8, 384, 2, True, False),    # four waves of 2 experts (Mixtral's form)
+    (30001, 7, 128, 3, False, True),    # E <= 8, a large batch, ragged last block
+    (8193, 16, 768, 4, True, False),    # 2 per lane in two sets of 32 tokens (DBRX's form)
+    (14000, 11, 192, 4, False, True),   # E <= 16 past ~13650 tokens: 4 per lane
+    (33, 16, 6144, 4, True, True),      # DBRX's width, one partial workgroup
+])
+def test_route_lane_shapes(T, E, H, k, renorm, use_bias):
+    """The lane-per-token router (E <= 16) in each of its shapes, picked by
+    expert count and batch size, with ragged token blocks, 1 to 96 stages
+    and the bias, against the oracle bit for bit."""
+    rng = np.random.default_rng(1000 + E + T)
+    xb = synth.bf16_bits(rng.standard_normal((T, H), dtype=np.float32))
+    wr = rng.standard_normal((E, H), dtype=np.float32) * np.float32(0.02)
+    bias = (rng.standard_normal(E, dtype=np.float32) * np.float32(0.1)) if use_bias else None
+    _, ids, w = oracle.route(xb, wr, bias, k, renorm)
+    d = moe.dims(T, H, 64, E, k, renormalize=renorm)
+    gids = torch.empty((T, k), dtype=torch.int32, device=dev())
+    gw = torch.empty((T, k), dtype=torch.float32, device=dev())
+    moe.route(d, bf16(xb), f32(wr), f32(bias) if use_bias else None, gids, gw)
+    torch.cuda.synchronize()
+    assert np.array_equal(gids.cpu().numpy(), ids)
+    assert weights_match(gw.cpu().numpy(), w)
+
+
 def test_route_ties_and_signed_zero():
     """Exact ties in the logits (duplicated router rows, zero rows) must go to
     the lower expert index, -0 and +0 being equal."""

@@ -40,9 +40,21 @@ __global__ __launch_bounds__(64) void hist_kernel(const int32_t *__restrict__ id
     __syncthreads();
     const int64_t base = (int64_t)blockIdx.x * kPermChunk;
     const uint64_t lt_mask = (1ull << lane) - 1ull;
-    for (int it = 0; it < kPermChunk / 64; ++it) {
+    // every id of the chunk is loaded before the first is ranked: one memory
+    // round trip per chunk instead of one per 64 slots
+    // (unconditional loads of a clamped slot, kept above the compiler
+    // barrier so that they are not sunk back to their uses)
+    constexpr int NIT = kPermChunk / 64;
+    int idv[NIT];
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) idv[it] = ids[min<int64_t>(base + it * 64 + lane, nslots - 1)];
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
         const int64_t s = base + it * 64 + lane;
-        const int e = s < nslots ? slot_bucket(ids, s, k, e0, EL, tps) : -1;
+        int e = idv[it] - e0;
+        if (s >= nslots || e < 0 || e >= EL) e = -1;
+        else if (tps > 0) e += (int)((uint32_t)s / (uint32_t)k / (uint32_t)tps) * EL;  // s < 2^31
         // lanes holding the same value (e + 1 in [0, 256], nine bits)
         const uint32_t v = (uint32_t)(e + 1);
         uint64_t match = ~0ull;

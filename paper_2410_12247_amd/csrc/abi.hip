@@ -214,10 +214,12 @@ moe_status moe_ffn_group(const moe_dims *dims, int32_t e_first, int32_t e_count,
     grid = std::max(8, (grid / 8) * 8);
     hipStream_t s = (hipStream_t)stream;
     // no workspace here: every tile covers the whole K range in one pass
+    // no expert has more rows than there are tokens
+    const int bm = group_tile_rows(dims->tokens);
     MOE_HIP(launch_group_gateup(*dims, e_first, e_count, offsets, x_perm, nullptr, w_gate, w_up,
-                                act, grid, nullptr, nullptr, group_tile_rows(), s));
+                                act, grid, nullptr, nullptr, bm, s));
     MOE_HIP(launch_group_down(*dims, e_first, e_count, offsets, act, w_down, y_perm, grid,
-                              nullptr, nullptr, group_tile_rows(), s));
+                              nullptr, nullptr, bm, s));
     return MOE_OK;
 }
 

@@ -130,8 +130,9 @@ hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, int64_t t
 // persistent grid may be cut along K (then a fixup kernel follows the GEMM
 // on the same stream); without them every tile is one pass over K.
 // Launches that share the scratch must not overlap.
-// bm: token rows of the tile (group_tile_rows() for a launch whose row
-// counts the host does not know; any valid_tile_rows value otherwise).
+// bm: token rows of the tile, any valid_tile_rows value (every height
+// gives the same bits in exact order); group_tile_rows picks it from a
+// bound on the experts' row counts.
 hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
                                const int32_t *offsets, const bf16_t *x_rows,
                                const int32_t *row_map, const bf16_t *w_gate,
@@ -159,7 +160,10 @@ int64_t gemm_tiles(int mode, int bm, int64_t rows, int N);
 double ffn_expert_us(int bm, int64_t rows, int H, int I, int grid, bool split);
 // The tile height the model prefers for a dense launch of `rows` rows.
 int dense_tile_rows(int64_t rows, int H, int I, int grid, bool split);
-int group_tile_rows();
+// The tile height of a grouped launch none of whose experts has more than
+// max_rows rows (the launch's tokens bound it: a token routes to an expert
+// at most once): 320, or the smallest height that holds max_rows below it.
+int group_tile_rows(int64_t max_rows);
 bool valid_tile_rows(int bm);
 
 }  // namespace moe

@@ -271,7 +271,9 @@ bool needs_host_counts(const moe_dims &d, const moe_opts &o) {
 // stage (or, with a fixed threshold m*, when every expert has >= m* rows).
 bool auto_picks_dense(const moe_dims &d, const moe_opts &o, const int32_t *rows, int n, int grid,
                       bool split, double *group_us, double *dense_us) {
-    const int bm_g = group_tile_rows();
+    int32_t max_rows = 0;
+    for (int e = 0; e < n; ++e) max_rows = std::max(max_rows, rows[e]);
+    const int bm_g = group_tile_rows(max_rows);
     int64_t tiles_gu = 0, tiles_dn = 0;
     double dus = 0.0;
     int32_t min_rows = INT32_MAX;
@@ -537,10 +539,10 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         shared_offsets_kernel<<<1, 64, 0, sm>>>(soff, (int32_t)T);
         MOE_HIP(hipGetLastError());
         MOE_HIP(launch_group_gateup(ds, 0, 1, soff, x, nullptr, shared_gate, shared_up,
-                                    shared_act, grid, split_part, split_meta, group_tile_rows(),
+                                    shared_act, grid, split_part, split_meta, group_tile_rows(T),
                                     sm));
         MOE_HIP(launch_group_down(ds, 0, 1, soff, shared_act, shared_down, y, grid, split_part,
-                                  split_meta, group_tile_rows(), sm));
+                                  split_meta, group_tile_rows(T), sm));
         MOE_TRY(tm.end(sm));
     }
 
@@ -591,10 +593,17 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         const int64_t t_lo = tok_stages ? std::min<int64_t>(T, i * tps) : 0;
         const int64_t t_hi = tok_stages ? std::min<int64_t>(T, (i + 1) * tps) : T;
         int64_t stage_rows = L.rcap;
+        // rows of the stage's largest expert: the stage's tokens bound it,
+        // the host counts give it exactly
+        int64_t stage_max_rows = t_hi - t_lo;
         bool dense = o->gemm_mode == MOE_GEMM_DENSE;
         if (need_counts) {
             stage_rows = 0;
-            for (int b = b0; b < b0 + per_stage; ++b) stage_rows += hc[b];
+            stage_max_rows = 0;
+            for (int b = b0; b < b0 + per_stage; ++b) {
+                stage_rows += hc[b];
+                stage_max_rows = std::max<int64_t>(stage_max_rows, hc[b]);
+            }
             if (o->gemm_mode == MOE_GEMM_AUTO)
                 dense = auto_picks_dense(d, *o, &hc[b0], per_stage, grid, split, nullptr,
                                          nullptr);
@@ -648,7 +657,7 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
             // read on the device
             if (timing) ++g_timing.group_stages;
             if (stage_rows > 0) {
-                const int bm = group_tile_rows();
+                const int bm = group_tile_rows(stage_max_rows);
                 MOE_TRY(tm.begin(sm, PH_GATEUP));
                 MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, xrows, rmap, w_gate, w_up,
                                             act, grid, split_part, split_meta, bm, sm));
@@ -738,9 +747,11 @@ moe_status moe_gemm_plan(const moe_dims *dims, const moe_opts *opts, int32_t n_e
     if (o->gemm_mode == MOE_GEMM_GROUP) d_ = false;
     if (o->gemm_mode == MOE_GEMM_DENSE) d_ = true;
     *dense = d_ ? 1 : 0;
+    int32_t max_rows = 0;
+    for (int e = 0; e < n_experts; ++e) max_rows = std::max(max_rows, rows[e]);
     if (tile_rows)
         for (int e = 0; e < n_experts; ++e)
-            tile_rows[e] = !d_ ? group_tile_rows()
+            tile_rows[e] = !d_ ? group_tile_rows(max_rows)
                            : rows[e] == 0 ? 0
                            : o->dense_tile_rows > 0
                                ? o->dense_tile_rows

@@ -1070,7 +1070,17 @@ int dense_tile_rows(int64_t rows, int H, int I, int grid, bool split) {
 #endif
 }
 
-int group_tile_rows() { return kTokenTile; }
+int group_tile_rows(int64_t max_rows) {
+#if MOE_GEMM_PINGPONG
+    // below the tallest tile, the smallest height that still holds every
+    // expert's rows in one tile: fewer padded rows, never more tiles
+    if (max_rows <= 128) return 128;
+    if (max_rows <= 192) return 192;
+    if (max_rows <= 256) return 256;
+#endif
+    (void)max_rows;
+    return kTokenTile;
+}
 
 bool valid_tile_rows(int bm) {
 #if MOE_GEMM_PINGPONG

@@ -246,6 +246,14 @@ def test_gemm_plan_model():
     assert dense == (dus < gus)
     # forced kinds
     assert plan(d, moe.opts(gemm_mode=moe.GEMM_GROUP), [4096])[:2] == (False, [320])
+    # a grouped launch's tile height: the smallest that holds its largest
+    # expert below 320 rows (decode batches), else 320
+    grouped = moe.opts(gemm_mode=moe.GEMM_GROUP)
+    assert plan(d, grouped, [1, 0])[1] == [128, 128]
+    assert plan(d, grouped, [128, 3])[1] == [128, 128]
+    assert plan(d, grouped, [129])[1] == [192]
+    assert plan(d, grouped, [200, 7])[1] == [256, 256]
+    assert plan(d, grouped, [100, 257])[1] == [320, 320]
     dense, tiles, _, _ = plan(d, moe.opts(gemm_mode=moe.GEMM_DENSE), [4096, 0, 17])
     assert dense and tiles[1] == 0 and tiles[0] > 0 and tiles[2] > 0
     dense, tiles, _, _ = plan(d, moe.opts(gemm_mode=moe.GEMM_DENSE, dense_tile_rows=192),

@@ -881,10 +881,11 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(const float *__restric
 }
 
 // Tile policy of each scheduler: the ping-pong tile, 256 weight rows by BM
-// token rows.  The grouped launch does not know its row counts on the host
-// and always takes the tallest tile (BM = 320, fewest LDS bytes per MFMA);
-// a dense launch knows its expert's rows and takes the height whose tile
-// count fills the grid best (dense_tile_rows).
+// token rows.  The grouped launch knows only a bound on its experts' rows
+// (the tokens, or the largest host count) and takes the tallest tile
+// (BM = 320, fewest LDS bytes per MFMA) unless a smaller height holds that
+// bound (group_tile_rows); a dense launch knows its expert's rows and takes
+// the height whose tile count fills the grid best (dense_tile_rows).
 #ifndef MOE_GEMM_PINGPONG
 #define MOE_GEMM_PINGPONG 1
 #endif

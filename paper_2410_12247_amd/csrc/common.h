@@ -86,10 +86,14 @@ constexpr int kPermChunk = 1024;
 
 // K split of the grouped GEMM's last, partial round of tiles: at most
 // kSplitMaxPieces pieces per tile, each at least kSplitMinStages K stages
-// long, at most kSplitSlots pieces (partial-accumulator buffers) in all, so
-// at most kSplitSlots / 2 tiles cut.
+// long (kSplitMinStagesAlone when the launch has fewer tiles than
+// workgroups: decode-sized launches, whose pieces would otherwise leave
+// most compute units idle while the weights stream), at most kSplitSlots
+// pieces (partial-accumulator buffers) in all, so at most kSplitSlots / 2
+// tiles cut.
 constexpr int kSplitMaxPieces = 8;
 constexpr int kSplitMinStages = 32;
+constexpr int kSplitMinStagesAlone = 8;
 constexpr int kSplitSlots = 256;
 constexpr int kSplitMetaInts = 2 + 4 * (kSplitSlots / 2);
 // Bytes of the partial-accumulator buffer the grouped GEMM takes (all slots).

@@ -736,7 +736,8 @@ __global__ __launch_bounds__(TP::THREADS) void group_kernel(
     const int rem = total - full;
     int S = 1;
     if (TP::CAN_SPLIT && parts != nullptr && rem > 0)
-        S = min(min(kSplitMaxPieces, G / rem), min(nk / kSplitMinStages, kSplitSlots / rem));
+        S = min(min(kSplitMaxPieces, G / rem),
+                min(nk / (full == 0 ? kSplitMinStagesAlone : kSplitMinStages), kSplitSlots / rem));
     if (S < 2) S = 1;
     if (split_meta != nullptr && slot == 0 && tid == 0) {
         split_meta[0] = S > 1 ? rem : 0;
@@ -1031,8 +1032,10 @@ double gemm_launch_us(int mode, int bm, int64_t tiles, int K, int grid, bool spl
     if (rem > 0) {
         int S = 1;
         if (split && 2 * rem <= grid)
-            S = (int)std::min<int64_t>(std::min<int64_t>(kSplitMaxPieces, grid / rem),
-                                       std::min<int64_t>(nk / kSplitMinStages, kSplitSlots / rem));
+            S = (int)std::min<int64_t>(
+                std::min<int64_t>(kSplitMaxPieces, grid / rem),
+                std::min<int64_t>(nk / (full_rounds == 0 ? kSplitMinStagesAlone : kSplitMinStages),
+                                  kSplitSlots / rem));
         const double busy = (double)std::min<int64_t>(grid, rem * std::max(S, 1)) / grid;
         const double part = kPartialRound[md] + (1.0 - kPartialRound[md]) * busy;
         if (S >= 2)

@@ -179,6 +179,19 @@ typedef struct {
  * or options. */
 size_t moe_workspace_bytes(const moe_dims *dims, const moe_opts *opts);
 
+/* Guard gaps of the workspace layout (a debugging aid for out-of-region
+ * writes; no passage of the paper defines it).  After every region of the
+ * layout moe_workspace_bytes() sizes, the library leaves MOE_WS_GUARD_BYTES
+ * bytes that no call reads or writes: a caller may fill them with a canary
+ * before a call and compare them after it.  Writes the byte offsets of the
+ * first `capacity` gaps (from the workspace start) to `offsets` and returns
+ * how many gaps the layout has; -1 for invalid dims or options, or for
+ * offsets == NULL with capacity > 0.  opts as in moe_workspace_bytes.
+ * Host-only; never touches the GPU. */
+#define MOE_WS_GUARD_BYTES 256
+int32_t moe_workspace_guards(const moe_dims *dims, const moe_opts *opts, int64_t *offsets,
+                             int32_t capacity);
+
 /* Router (the topKGating operator of Sec. 3.3; k of E experts per token as
  * in Sec. 3.2).  For each token t:
  *   z[e] = fp32 fused-multiply-add chain over h = 0..H-1 (ascending, from

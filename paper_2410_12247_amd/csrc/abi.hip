@@ -78,6 +78,8 @@ WsLayout ws_layout(const moe_dims *d, const moe_opts *opt) {
     auto take = [&](size_t bytes) {
         const size_t at = o;
         o = align_up(o + bytes);
+        if (L.nguards < kMaxWsGuards) L.guard[L.nguards++] = o;
+        o += kWsGuardBytes;
         return at;
     };
     L.chunk_counts = take(sizeof(int32_t) * L.nchunks * NB);
@@ -148,6 +150,19 @@ size_t moe_workspace_bytes(const moe_dims *dims, const moe_opts *opts) {
     if (check_dims(dims) != MOE_OK) return 0;
     if (opts && forward_buckets(dims, opts) <= 0) return 0;
     return ws_layout(dims, opts).total;
+}
+
+int32_t moe_workspace_guards(const moe_dims *dims, const moe_opts *opts, int64_t *offsets,
+                             int32_t capacity) {
+    if (check_dims(dims) != MOE_OK) return -1;
+    if (opts && forward_buckets(dims, opts) <= 0) return -1;
+    if (capacity < 0 || (capacity > 0 && !offsets)) {
+        fail(MOE_ERR_INVALID, "moe_workspace_guards: offsets NULL or capacity < 0");
+        return -1;
+    }
+    const WsLayout L = ws_layout(dims, opts);
+    for (int i = 0; i < L.nguards && i < capacity; ++i) offsets[i] = (int64_t)L.guard[i];
+    return L.nguards;
 }
 
 moe_status moe_route(const moe_dims *dims, const moe_bf16 *x, const float *w_router,

@@ -46,6 +46,10 @@ int device_cu_count();
 // Workspace layout used by moe_permute and moe_ffn_forward.  The dispatch
 // orders rows by a bucket index: the local expert (EXPERTS stages) or
 // token-range stage * EL + local expert (TOKENS stages); nbuckets of them.
+// Bytes left untouched after every workspace region (a canary a caller may
+// check for writes past a region), and the most regions a layout has.
+constexpr size_t kWsGuardBytes = 256;
+constexpr int kMaxWsGuards = 24;
 struct WsLayout {
     size_t chunk_counts;  // int32 [nchunks][nbuckets]
     size_t chunk_base;    // int32 [nchunks][nbuckets]
@@ -70,6 +74,9 @@ struct WsLayout {
     int64_t nchunks;
     int64_t rcap;
     int nbuckets;
+    // guard gaps of kWsGuardBytes after every region, never touched
+    size_t guard[kMaxWsGuards];
+    int nguards;
 };
 // Layout for moe_permute (o == NULL) or for moe_ffn_forward with options o
 // (valid options: check them first).

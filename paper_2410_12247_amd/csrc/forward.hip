@@ -24,6 +24,10 @@
 #include <mutex>
 #include <vector>
 
+#include <cstdio>
+
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "common.h"
 
 namespace moe {
@@ -431,6 +435,17 @@ moe_status check_tensors(const moe_dims &d, const moe_bf16 *x, const float *w_ro
 // The forward itself, after argument checks: workspace at `base` laid out
 // as L.  st == NULL (the no-allocation entry point) runs every step on the
 // caller's stream and never needs the row counts on the host.
+// A roctx range over the host-side enqueue of one part of the forward (the
+// whole call, the shared FFN, routing, dispatch, the wait for the row
+// counts, each pipeline stage), shown by rocprofv3 --marker-trace beside the
+// kernels; the calls cost next to nothing when no tool listens.
+struct Marker {
+    explicit Marker(const char *what) { roctxRangePushA(what); }
+    ~Marker() { roctxRangePop(); }
+    Marker(const Marker &) = delete;
+    Marker &operator=(const Marker &) = delete;
+};
+
 moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *x,
                         const float *w_router, const float *bias, const moe_bf16 *w_gate,
                         const moe_bf16 *w_up, const moe_bf16 *w_down,
@@ -510,6 +525,7 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
     const int H = d.hidden, I = d.inter;
     const int64_t T = d.tokens;
 
+    Marker mark_all("moe_ffn_forward");
     int total_span = -1;
     MOE_TRY(tm.begin(s0, PH_TOTAL, &total_span));
     // shared experts: independent of routing, start at once on the GEMM stream
@@ -530,6 +546,7 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         // grouped scheduler, whose K split shortens a partial last round of
         // tiles (e.g. 1040 down tiles on 256 workgroups); same tile code, so
         // the same bits as a dense launch under MOE_FLAG_EXACT_ORDER
+        Marker mark("moe shared FFN");
         moe_dims ds = d;
         ds.inter = d.shared_inter;
         ds.local_begin = 0;
@@ -547,19 +564,27 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
     }
 
     // routing and dispatch indices on the caller stream
-    MOE_TRY(tm.begin(s0, PH_ROUTE));
-    float *logits = L.logits ? reinterpret_cast<float *>(base + L.logits) : nullptr;
-    MOE_HIP(launch_route(d, x, w_router, bias, ids, wts, logits, s0));
-    MOE_TRY(tm.end(s0));
-    MOE_TRY(tm.begin(s0, PH_PERMUTE));
-    MOE_HIP(launch_permute(d, ids, base, L, tps, cnt, off, cnt_el, sorted_slot, slot_row, s0));
-    MOE_TRY(tm.end(s0));
+    {
+        Marker mark("moe route");
+        MOE_TRY(tm.begin(s0, PH_ROUTE));
+        float *logits = L.logits ? reinterpret_cast<float *>(base + L.logits) : nullptr;
+        MOE_HIP(launch_route(d, x, w_router, bias, ids, wts, logits, s0));
+        MOE_TRY(tm.end(s0));
+    }
+    {
+        Marker mark("moe dispatch");
+        MOE_TRY(tm.begin(s0, PH_PERMUTE));
+        MOE_HIP(launch_permute(d, ids, base, L, tps, cnt, off, cnt_el, sorted_slot, slot_row,
+                               s0));
+        MOE_TRY(tm.end(s0));
+    }
 
     // GEMM kind per stage needs the row counts on the host
     std::vector<int32_t> hc;
     const bool need_counts = needs_host_counts(d, *o);
     if (need_counts) {
         if (!st) return fail(MOE_ERR_UNSUPPORTED, "row counts needed on the host");
+        Marker mark("moe row counts to host");
         MOE_HIP(hipMemcpyAsync(st->pinned_counts, cnt, sizeof(int32_t) * NB,
                                hipMemcpyDeviceToHost, s0));
         MOE_HIP(hipEventRecord(ev_counts, s0));
@@ -608,6 +633,10 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
                 dense = auto_picks_dense(d, *o, &hc[b0], per_stage, grid, split, nullptr,
                                          nullptr);
         }
+        char stage_name[64];
+        snprintf(stage_name, sizeof(stage_name), "moe stage %d of %d (%s)", i + 1, PN,
+                 dense ? "dense" : "group");
+        Marker mark(stage_name);
         // gather (dispatch of this stage), unless the gate/up GEMM reads its
         // token rows straight from x through sorted_slot
         const bool fold_gather = fold_ok;

@@ -21,7 +21,7 @@ CHUNK_EXPERTS, CHUNK_TOKENS = 0, 1
 FLAG_TIMING, FLAG_TIMING_GEMM, FLAG_EXACT_ORDER, FLAG_SERIAL = 1, 2, 4, 8
 
 # the entry points include/moe.h declares
-EXPORTS = ("moe_workspace_bytes", "moe_route", "moe_permute", "moe_gather", "moe_ffn_group",
+EXPORTS = ("moe_workspace_bytes", "moe_workspace_guards", "moe_route", "moe_permute", "moe_gather", "moe_ffn_group",
            "moe_ffn_dense", "moe_combine", "moe_ffn_forward", "moe_ffn_forward_noalloc",
            "moe_last_timing",
            "moe_gemm_plan", "moe_pipeline_plan", "moe_choose_pipeline_n", "moe_status_string",
@@ -84,6 +84,8 @@ def lib():
     D, O = ctypes.POINTER(Dims), ctypes.POINTER(Opts)
     L.moe_workspace_bytes.argtypes = [D, O]
     L.moe_workspace_bytes.restype = SZ
+    L.moe_workspace_guards.argtypes = [D, O, ctypes.POINTER(ctypes.c_int64), ctypes.c_int32]
+    L.moe_workspace_guards.restype = ctypes.c_int32
     L.moe_route.argtypes = [D, P, P, P, P, P, P]
     L.moe_permute.argtypes = [D, P, P, P, P, P, P, P, P, SZ, P]
     L.moe_gather.argtypes = [D, I32, I32, P, P, P, P, P]
@@ -159,6 +161,20 @@ def _s(stream):
 
 def workspace_bytes(d: Dims, o: Optional[Opts] = None) -> int:
     return lib().moe_workspace_bytes(ctypes.byref(d), ctypes.byref(o) if o is not None else None)
+
+
+WS_GUARD_BYTES = 256  # MOE_WS_GUARD_BYTES
+
+
+def workspace_guards(d: Dims, o: Optional[Opts] = None) -> list:
+    """Byte offsets of the workspace's guard gaps (WS_GUARD_BYTES each)."""
+    ob = ctypes.byref(o) if o is not None else None
+    n = lib().moe_workspace_guards(ctypes.byref(d), ob, None, 0)
+    if n < 0:
+        raise MoEError(1, "moe_workspace_guards: invalid dims or options")
+    buf = (ctypes.c_int64 * max(n, 1))()
+    lib().moe_workspace_guards(ctypes.byref(d), ob, buf, n)
+    return list(buf[:n])
 
 
 def route(d, x, w_router, bias, topk_ids, topk_w, stream=None):

@@ -29,3 +29,22 @@ def assert_close(got: np.ndarray, ref: np.ndarray, what: str,
     assert err <= max_abs and rel <= rel_fro, \
         f"{what}: max-abs {err:.3g} (<= {max_abs}), rel-frobenius {rel:.3g} (<= {rel_fro})"
     return err, rel
+
+
+# workspace canary: the byte the guard gaps are filled with before a call
+CANARY = 0xA5
+
+
+def canary_fill(ws: torch.Tensor):
+    ws.fill_(CANARY)
+
+
+def assert_guards(ws: torch.Tensor, guards, what: str):
+    """Every guard gap of the workspace still holds the canary."""
+    from paper_2410_12247_amd import moe
+    torch.cuda.synchronize()
+    for off in guards:
+        gap = ws[off:off + moe.WS_GUARD_BYTES]
+        assert gap.numel() == moe.WS_GUARD_BYTES, f"{what}: guard at {off} past the workspace"
+        bad = int((gap != CANARY).sum())
+        assert bad == 0, f"{what}: {bad} bytes of the guard gap at offset {off} written"

@@ -231,6 +231,35 @@ def test_noalloc_forward_rejects_on_the_host():
     assert call(zero, moe.opts()) == 0
 
 
+def test_workspace_guards_layout():
+    """Guard gaps (moe_workspace_guards): one after every region, in order,
+    inside the workspace, the last one ending it; regions never overlap a
+    gap; invalid dims are refused."""
+    L = moe.lib()
+    G = moe.WS_GUARD_BYTES
+    for d, o in [(moe.dims(16384, 4096, 3584, 8, 2), moe.opts()),
+                 (moe.dims(16384, 5120, 1536, 160, 6, 0, 20, False, 3072), moe.opts()),
+                 (moe.dims(300, 256, 128, 8, 2), moe.opts(exact_order=True)),
+                 (moe.dims(1500, 192, 320, 4, 2), moe.opts(pipeline_n=2,
+                                                           chunk_mode=moe.CHUNK_TOKENS)),
+                 (moe.dims(777, 512, 384, 16, 4, 3, 5), None)]:
+        guards = moe.workspace_guards(d, o)
+        total = moe.workspace_bytes(d, o)
+        assert len(guards) >= (3 if o is None else 15)
+        assert guards[0] > 0
+        assert all(b >= a + G for a, b in zip(guards, guards[1:]))
+        assert guards[-1] + G == total
+        assert all(g % 256 == 0 for g in guards)
+    # capacity smaller than the count: the first offsets, and the full count
+    d = moe.dims(16384, 4096, 3584, 8, 2)
+    buf = (ctypes.c_int64 * 2)()
+    n = L.moe_workspace_guards(ctypes.byref(d), None, buf, 2)
+    assert n == 3 and list(buf) == moe.workspace_guards(d)[:2]
+    with pytest.raises(moe.MoEError):
+        moe.workspace_guards(moe.dims(16, 100, 64, 8, 2))  # hidden not a multiple of 64
+    assert L.moe_workspace_guards(ctypes.byref(d), None, None, 4) == -1
+
+
 def test_gemm_plan_model():
     """AUTO's GroupGemm / DenseGemm plan for one stage (moe_gemm_plan, host
     only): forced modes, per-expert tile heights among the built ones, an

@@ -8,7 +8,7 @@ import torch
 import oracle
 from paper_2410_12247_amd import moe, synth
 
-from gpu_util import Dev, assert_close, bf16, bits, dev, f32, i32
+from gpu_util import Dev, assert_close, assert_guards, bf16, bits, canary_fill, dev, f32, i32
 
 pytestmark = pytest.mark.gpu
 
@@ -161,6 +161,31 @@ def test_route_lane_shapes(T, E, H, k, renorm, use_bias):
     torch.cuda.synchronize()
     assert np.array_equal(gids.cpu().numpy(), ids)
     assert weights_match(gw.cpu().numpy(), w)
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("tiny", {}),
+    ("fine", {}),                                          # shared experts, no renorm
+    ("ragged8", dict(gemm_mode=moe.GEMM_DENSE)),           # dense launches, host counts
+    ("split4", {}),                                        # K-split partials and fixup
+    ("window", dict(pipeline_n=5, exact_order=True)),      # one expert per stage
+    ("tall4", dict(pipeline_n=2, chunk_mode=moe.CHUNK_TOKENS, timing=True)),
+])
+def test_workspace_guards_untouched(name, kw):
+    """Canary-filled guard gaps around every workspace region hold the
+    canary after two forwards under each option set (no kernel writes past
+    its region), and the forward still routes as the oracle does."""
+    inp, ids, _ = case(name)
+    g = Dev(inp)
+    o = moe.opts(**kw)
+    guards = moe.workspace_guards(g.d, o)
+    assert len(guards) >= 15
+    buf = g.buffers(o)
+    canary_fill(buf.ws)
+    g.run(buf)
+    g.run(buf)
+    assert_guards(buf.ws, guards, name)
+    assert np.array_equal(buf.topk_ids.cpu().numpy(), ids)
 
 
 def test_route_ties_and_signed_zero():

@@ -11,7 +11,7 @@ import torch
 import oracle
 from paper_2410_12247_amd import moe, synth
 
-from gpu_util import Dev, assert_close
+from gpu_util import Dev, assert_close, assert_guards, canary_fill
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -47,7 +47,11 @@ def test_full_workload(name, T):
     shp = _shape(name, T)
     inp = synth.make_inputs(shp)
     g = Dev(inp)
-    buf = g.forward(moe.opts(gemm_mode=moe.GEMM_AUTO, pipeline_n=1))
+    o = moe.opts(gemm_mode=moe.GEMM_AUTO, pipeline_n=1)
+    buf = g.buffers(o)
+    canary_fill(buf.ws)
+    g.run(buf)
+    assert_guards(buf.ws, moe.workspace_guards(g.d, o), f"{name} T={shp.T} forward")
     ids_g = buf.topk_ids.cpu().numpy()
     w_g = buf.topk_w.cpu().numpy()
     y = buf.y
@@ -66,8 +70,9 @@ def test_full_workload(name, T):
     gss = torch.full((shp.T * min(shp.k, shp.EL),), -7, dtype=torch.int32, device=y.device)
     gsr = torch.empty(shp.T * shp.k, dtype=torch.int32, device=y.device)
     ws = torch.empty(moe.workspace_bytes(g.d), dtype=torch.uint8, device=y.device)
+    canary_fill(ws)
     moe.permute(g.d, buf.topk_ids, None, gc, go, gss, gsr, None, ws)
-    torch.cuda.synchronize()
+    assert_guards(ws, moe.workspace_guards(g.d), f"{name} T={shp.T} permute")
     assert np.array_equal(gc.cpu().numpy(), counts)
     assert np.array_equal(go.cpu().numpy(), offsets)
     assert np.array_equal(gss.cpu().numpy()[:R], sorted_slot)

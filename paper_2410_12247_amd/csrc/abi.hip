@@ -233,8 +233,15 @@ moe_status moe_ffn_group(const moe_dims *dims, int32_t e_first, int32_t e_count,
     const int bm = group_tile_rows(dims->tokens);
     MOE_HIP(launch_group_gateup(*dims, e_first, e_count, offsets, x_perm, nullptr, w_gate, w_up,
                                 act, grid, nullptr, nullptr, bm, s));
-    MOE_HIP(launch_group_down(*dims, e_first, e_count, offsets, act, w_down, y_perm, grid,
-                              nullptr, nullptr, bm, s));
+    // decode-sized experts with enough tiles: the skinny down tile
+    const int64_t active = std::min<int64_t>(e_count, dims->tokens * dims->top_k);
+    const int sk = skinny_down_rows(dims->tokens, active, dims->hidden);
+    if (sk > 0)
+        MOE_HIP(launch_skinny_down(*dims, e_first, e_count, offsets, act, w_down, y_perm, sk,
+                                   active, s));
+    else
+        MOE_HIP(launch_group_down(*dims, e_first, e_count, offsets, act, w_down, y_perm, grid,
+                                  nullptr, nullptr, bm, s));
     return MOE_OK;
 }
 

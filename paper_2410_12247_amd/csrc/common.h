@@ -175,6 +175,19 @@ int dense_tile_rows(int64_t rows, int H, int I, int grid, bool split);
 // max_rows rows (the launch's tokens bound it: a token routes to an expert
 // at most once): 320, or the smallest height that holds max_rows below it.
 int group_tile_rows(int64_t max_rows);
+// Skinny down GEMM for decode-sized grouped launches: one wave per tile of
+// 64 output columns by an expert's rows (at most 64) over the whole K
+// range, no K split (the same bits as every other tile height in exact
+// order).  skinny_down_rows gives the tile's rows (16, 32 or 64) for a
+// launch whose experts have at most max_rows rows, of which at most
+// active_experts have any, with N output columns; 0 where the skinny tile
+// does not apply: more rows, or fewer than two tiles per compute unit (the
+// general tile's K split then keeps more loads in flight).
+constexpr int64_t kSkinnyMaxRows = 64;
+int skinny_down_rows(int64_t max_rows, int64_t active_experts, int N);
+hipError_t launch_skinny_down(const moe_dims &d, int e_first, int e_count,
+                              const int32_t *offsets, const bf16_t *act, const bf16_t *w_down,
+                              float *y_perm, int bm, int64_t active_experts, hipStream_t s);
 bool valid_tile_rows(int bm);
 
 }  // namespace moe

@@ -691,9 +691,17 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
                 MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, xrows, rmap, w_gate, w_up,
                                             act, grid, split_part, split_meta, bm, sm));
                 MOE_TRY(tm.end(sm));
+                // decode-sized stages with enough tiles: the skinny down tile
+                const int64_t active =
+                    std::min<int64_t>(per_stage, (t_hi - t_lo) * (int64_t)d.top_k);
+                const int sk = skinny_down_rows(stage_max_rows, active, H);
                 MOE_TRY(tm.begin(sm, PH_DOWN));
-                MOE_HIP(launch_group_down(d, e_w, per_stage, goff, act, w_down, y_perm, grid,
-                                          split_part, split_meta, bm, sm));
+                if (sk > 0)
+                    MOE_HIP(launch_skinny_down(d, e_w, per_stage, goff, act, w_down, y_perm, sk,
+                                               active, sm));
+                else
+                    MOE_HIP(launch_group_down(d, e_w, per_stage, goff, act, w_down, y_perm, grid,
+                                              split_part, split_meta, bm, sm));
                 MOE_TRY(tm.end(sm));
                 if (timing) {
                     ++g_timing.gateup_launches;

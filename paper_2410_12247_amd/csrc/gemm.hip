@@ -899,6 +899,190 @@ template <int MODE, int BM = kTokenTile> using TileOf = FourWave<MODE, 256, 256,
 #endif
 template <int MODE> using GroupTile = TileOf<MODE>;
 
+// ---------------------------------------------------------------------------
+// Skinny down tile for decode-sized grouped launches: every expert of the
+// launch has at most BM (16, 32 or 64) rows, so its down GEMM is one row of
+// tiles that streams the expert's weights once.  A workgroup is one wave
+// and owns SK_BN output columns (weight rows) by the expert's rows over the
+// whole K range: no K split, no fixup.  Weight and act rows stream through
+// a ring of LDS stages of 32 K by LDS-DMA, all but one stage ahead, the
+// chunks placed as in the ping-pong tile.  The ring depth is chosen per
+// launch (dynamic LDS): the deepest with which every tile of the launch is
+// resident at once (a second, partial round of tiles would take as long as
+// the first).  The MFMA (16x16x32 bf16, the weight fragment as the A
+// operand, K ascending from 0) and the fragment contents are the ping-pong
+// tile's, so the outputs carry the same bits as every other tile height in
+// exact order.  The fragment reads and their wait are one assembly block:
+// the compiler would otherwise wait for all LDS-DMA in flight before
+// reading LDS and drain the ring every stage.
+constexpr int SK_BN = 64;  // weight rows (output columns) per tile
+constexpr int SK_BK = 32;
+constexpr int SK_NS_MAX = 16;             // ring stages at most
+constexpr size_t SK_LDS_MAX = 64 * 1024;  // dynamic LDS of one workgroup at most
+
+// stages a wave can keep ahead: vmcnt counts at most 63 requests
+constexpr int sk_ahead_max(int lps) { return std::min(SK_NS_MAX - 1, 63 / lps); }
+
+// LDS bytes of a workgroup with a ring of ns stages: the ring plus room for
+// the act-fragment reads a tile of fewer than 64 rows does not use
+constexpr size_t sk_lds_bytes(int bm, int ns) {
+    return (size_t)ns * (SK_BN + bm) * SK_BK * 2 + (size_t)(4 - bm / 16) * 1024;
+}
+
+// the stage's fragments: 4 weight fragments from wa, 4 act fragments from
+// xa (a tile of fewer rows reads the first ones; the others land in the
+// next slot or the padding after the ring), 1024 bytes apart
+__device__ __forceinline__ void sk_read_frags(bf16x8 (&f)[8], uint32_t wa, uint32_t xa) {
+    asm volatile(
+        "ds_read_b128 %0, %8\n\t"
+        "ds_read_b128 %1, %8 offset:1024\n\t"
+        "ds_read_b128 %2, %8 offset:2048\n\t"
+        "ds_read_b128 %3, %8 offset:3072\n\t"
+        "ds_read_b128 %4, %9\n\t"
+        "ds_read_b128 %5, %9 offset:1024\n\t"
+        "ds_read_b128 %6, %9 offset:2048\n\t"
+        "ds_read_b128 %7, %9 offset:3072\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(f[0]), "=&v"(f[1]), "=&v"(f[2]), "=&v"(f[3]), "=&v"(f[4]), "=&v"(f[5]),
+          "=&v"(f[6]), "=&v"(f[7])
+        : "v"(wa), "v"(xa)
+        : "memory");
+}
+
+// s_waitcnt vmcnt(LPS * n), 0 <= n <= K
+template <int LPS, int K = sk_ahead_max(LPS)>
+__device__ __forceinline__ void sk_wait(int n) {
+    if (n == K) {
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(K * LPS) : "memory");
+    } else if constexpr (K > 0) {
+        sk_wait<LPS, K - 1>(n);
+    }
+}
+
+// y[r0 + r][n0 .. n0 + 63] = w_down[e_first + e][n0 ..] . act[r0 + r] for
+// the r < rows of expert e (offsets indexed by e_first + e, as in the other
+// launches); grid = e_count * (N / SK_BN), ns ring stages.
+template <int BM>
+__global__ __launch_bounds__(64) void skinny_down_kernel(const int32_t *__restrict__ offsets,
+                                                         int e_first, int e_count,
+                                                         const bf16_t *__restrict__ act,
+                                                         const bf16_t *__restrict__ w,
+                                                         int64_t wstride, int N, int K,
+                                                         float *__restrict__ y, int ns) {
+    constexpr int BK = SK_BK;
+    constexpr int TN = SK_BN / 16, TM = BM / 16;
+    static_assert(TM <= 4, "at most 4 act fragments per stage");
+    constexpr int WI = SK_BN / 16, XI = BM / 16;  // LDS-DMA requests (16 rows x 64 bytes)
+    constexpr int LPS = WI + XI;
+    constexpr int STAGE = (SK_BN + BM) * BK;  // bf16 elements
+    // ring of ns stages (2 <= ns <= sk_ahead_max(LPS) + 1), sk_lds_bytes
+    extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+
+    const int NT = N / SK_BN;
+    const int e = blockIdx.x / NT;
+    const int nt = blockIdx.x - e * NT;
+    if (e >= e_count) return;
+    const int r0 = offsets[e_first + e];
+    const int rows = offsets[e_first + e + 1] - r0;  // <= BM (the launcher's bound)
+    if (rows <= 0) return;
+    const int lane = threadIdx.x;
+    const int64_t n0 = (int64_t)nt * SK_BN;
+
+    // LDS-DMA sources: lane i fetches row (i / 4) of a 16-row request, the
+    // 16-byte chunk (i % 4) ^ swz(row) of the stage's 32 K, into place i % 4
+    const int drow = lane >> 2;
+    const int dchunk = ((lane & 3) ^ swz<BK>(drow)) * 8;
+    const bf16_t *src[LPS];
+    const bf16_t *we = w + (int64_t)(e_first + e) * wstride;
+#pragma unroll
+    for (int i = 0; i < WI; ++i) src[i] = we + (n0 + i * 16 + drow) * K + dchunk;
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+        const int j = min(i * 16 + drow, rows - 1);  // rows past the expert's: repeats
+        src[WI + i] = act + (int64_t)(r0 + j) * K + dchunk;
+    }
+    const int nk = K / BK;
+    auto issue = [&](int kt, int slot) {
+        bf16_t *sb = smem + slot * STAGE;
+#pragma unroll
+        for (int i = 0; i < LPS; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void_t *)(src[i] + kt * BK),
+                                             (lds_void_t *)(sb + i * 16 * BK), 16, 0, 0);
+    };
+
+    // fragment addresses in ring slot 0: weight row t * 16 + lrow and act
+    // row m * 16 + lrow, the chunk holding K 8 (lane / 16) .. + 7
+    const int lrow = lane & 15;
+    const int chunk = ((lane >> 4) ^ swz<BK>(lrow)) * 8;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void_t *)smem;
+    const uint32_t wa0 = lds0 + (uint32_t)((lrow * BK + chunk) * 2);
+    const uint32_t xa0 = wa0 + (uint32_t)(SK_BN * BK * 2);
+
+    floatx4 acc[TN][TM];
+#pragma unroll
+    for (int t = 0; t < TN; ++t)
+#pragma unroll
+        for (int m = 0; m < TM; ++m) acc[t][m] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // stage kt goes to ring slot kt % ns
+    const int ahead = ns - 1;
+    for (int kt = 0; kt < min(ahead, nk); ++kt) issue(kt, kt);
+    int wslot = ahead, rslot = 0;  // slots of stages kt + ahead and kt
+    for (int kt = 0; kt < nk; ++kt) {
+        // stage kt + ahead into the slot read at kt - 1
+        if (kt + ahead < nk) issue(kt + ahead, wslot);
+        wslot = wslot + 1 == ns ? 0 : wslot + 1;
+        sk_wait<LPS>(min(ahead, nk - 1 - kt));  // stage kt landed
+        const uint32_t so = (uint32_t)(rslot * STAGE * 2);
+        rslot = rslot + 1 == ns ? 0 : rslot + 1;
+        bf16x8 f[8];
+        sk_read_frags(f, wa0 + so, xa0 + so);
+#pragma unroll
+        for (int m = 0; m < TM; ++m)
+#pragma unroll
+            for (int t = 0; t < TN; ++t)
+                acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f[t], f[4 + m], acc[t][m],
+                                                                    0, 0, 0);
+    }
+
+    // epilogue: the lane holds output columns t * 16 + 4 (lane / 16) .. + 3
+    // of row m * 16 + (lane % 16)
+    const int ocol = (lane >> 4) * 4;
+#pragma unroll
+    for (int m = 0; m < TM; ++m) {
+        const int row = m * 16 + lrow;
+        if (row >= rows) continue;
+        float *o = y + (int64_t)(r0 + row) * N + n0;
+#pragma unroll
+        for (int t = 0; t < TN; ++t) *reinterpret_cast<floatx4 *>(o + t * 16 + ocol) = acc[t][m];
+    }
+}
+
+// Ring depth of a launch of `tiles` non-empty tiles: the deepest ring (at
+// most sk_ahead_max + 1 stages, SK_LDS_MAX bytes) with which the tiles of a
+// compute unit all fit its LDS at once, and at least 4 stages.
+int sk_ring(int bm, int64_t tiles) {
+    const int lps = SK_BN / 16 + bm / 16;
+    const int cus = device_cu_count();
+    const int64_t per_cu = std::max<int64_t>(1, (tiles + cus - 1) / cus);
+    const size_t cap = std::min<size_t>(SK_LDS_MAX, (size_t)(160 * 1024) / per_cu);
+    int ns = sk_ahead_max(lps) + 1;
+    while (ns > 4 && sk_lds_bytes(bm, ns) > cap) --ns;
+    return ns;
+}
+
+template <int BM>
+hipError_t skinny_down_launch(unsigned blocks, int ns, const int32_t *offsets, int e_first,
+                              int e_count, const bf16_t *act, const bf16_t *w, int64_t wstride,
+                              int N, int K, float *y, hipStream_t s) {
+    constexpr int LPS = SK_BN / 16 + BM / 16;
+    if (ns < 2 || ns - 1 > sk_ahead_max(LPS) || sk_lds_bytes(BM, ns) > SK_LDS_MAX)
+        return hipErrorInvalidValue;
+    skinny_down_kernel<BM><<<blocks, 64, sk_lds_bytes(BM, ns), s>>>(
+        offsets, e_first, e_count, act, w, wstride, N, K, y, ns);
+    return hipGetLastError();
+}
+
 int round_grid(int64_t tiles) { return (int)(((tiles + NXCD - 1) / NXCD) * NXCD); }
 
 // Fixup launch after a grouped GEMM that was given a split buffer: at most
@@ -1131,6 +1315,37 @@ hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
     return group_launch_bm<1>(bm, offsets, e_first, e_count, act, nullptr, 1, w_down, nullptr,
                               (int64_t)d.hidden * d.inter, d.hidden, d.inter, y_perm, d.hidden,
                               grid, parts, split_meta, s);
+}
+
+int skinny_down_rows(int64_t max_rows, int64_t active_experts, int N) {
+    if (max_rows > kSkinnyMaxRows || N % SK_BN) return 0;
+    if (active_experts * (N / SK_BN) < 2 * (int64_t)device_cu_count()) return 0;
+    return max_rows <= 16 ? 16 : max_rows <= 32 ? 32 : 64;
+}
+
+hipError_t launch_skinny_down(const moe_dims &d, int e_first, int e_count,
+                              const int32_t *offsets, const bf16_t *act, const bf16_t *w_down,
+                              float *y_perm, int bm, int64_t active_experts, hipStream_t s) {
+    if (e_count <= 0) return hipSuccess;
+    const int N = d.hidden, K = d.inter;
+    if (N % SK_BN || K % SK_BK) return hipErrorInvalidValue;
+    const unsigned blocks = (unsigned)(e_count * (N / SK_BN));
+    const int64_t active = std::min<int64_t>(e_count, std::max<int64_t>(1, active_experts));
+    const int ns = sk_ring(bm, active * (N / SK_BN));
+    const int64_t wstride = (int64_t)N * K;
+    switch (bm) {
+        case 16:
+            return skinny_down_launch<16>(blocks, ns, offsets, e_first, e_count, act, w_down,
+                                          wstride, N, K, y_perm, s);
+        case 32:
+            return skinny_down_launch<32>(blocks, ns, offsets, e_first, e_count, act, w_down,
+                                          wstride, N, K, y_perm, s);
+        case 64:
+            return skinny_down_launch<64>(blocks, ns, offsets, e_first, e_count, act, w_down,
+                                          wstride, N, K, y_perm, s);
+        default:
+            return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace moe

@@ -188,6 +188,63 @@ def test_workspace_guards_untouched(name, kw):
     assert np.array_equal(buf.topk_ids.cpu().numpy(), ids)
 
 
+# Decode-sized shapes whose grouped down GEMM takes the skinny tile (at most
+# 64 rows per expert, at least two 64-column tiles per compute unit of a
+# 256-CU device): tile rows 16, 32 and 64, K shorter than the LDS ring,
+# a local window whose later pipeline stages start at expert e_first > 0.
+@pytest.mark.parametrize("T,E,EL,e0,k,H,I,shared", [
+    (5, 64, 64, 0, 8, 1024, 256, 0),      # 16-row tiles
+    (64, 8, 8, 0, 2, 4096, 256, 0),       # 32-row tiles
+    (64, 4, 4, 0, 2, 8192, 128, 0),       # 64-row tiles; 4 K stages
+    (64, 2, 2, 0, 2, 16384, 64, 0),       # every expert exactly 64 rows
+    (48, 32, 16, 8, 8, 4096, 128, 0),     # a local window; PN = 2 stays skinny
+    (40, 160, 160, 0, 6, 512, 256, 512),  # many experts, most empty; shared FFN
+])
+def test_skinny_down_gemm(T, E, EL, e0, k, H, I, shared):
+    """The skinny down tile: output within the tolerance of the oracle, and
+    in exact order the same bits as per-expert dense launches of the general
+    tile, for any pipeline number and through moe_ffn_group."""
+    shp = C(name=f"skinny{T}_{E}", index=219, T=T, H=H, I=I, E=E, EL=EL, e0=e0, k=k,
+            renorm=True, n_shared=1 if shared else 0, Is=shared)
+    inp = synth.make_inputs(shp)
+    _, ids, w = oracle.route(inp.x, inp.w_router, inp.bias, k, True)
+    g = Dev(inp)
+    buf = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP, exact_order=True))
+    assert np.array_equal(buf.topk_ids.cpu().numpy(), ids)
+    y = buf.y.clone()
+    assert_close(y.cpu().numpy(), oracle_y(inp, ids, w, np.arange(T)), f"skinny T={T} E={E}")
+    dense = g.forward(moe.opts(gemm_mode=moe.GEMM_DENSE, exact_order=True)).y
+    assert torch.equal(y, dense), "skinny grouped and dense forwards differ"
+    # default options: the gate/up GEMM may cut its last round along K
+    assert_close(g.forward(moe.opts()).y.cpu().numpy(), y.cpu().numpy(), "default options",
+                 2e-3, 1e-4)
+    # pipelined stages: every stage after the first starts at expert e_first > 0
+    for pn in [p for p in (2, 4) if EL % p == 0]:
+        yp = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP, pipeline_n=pn, exact_order=True)).y
+        assert torch.equal(yp, y), f"PN={pn} differs"
+    if 2 * EL <= 256:  # token-range stages take PN * EL dispatch buckets
+        yt = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP, pipeline_n=2, exact_order=True,
+                                chunk_mode=moe.CHUNK_TOKENS)).y
+        assert torch.equal(yt, y), "token-range stages differ"
+    # moe_ffn_group over gathered rows against per-expert dense launches
+    counts, offsets, sorted_slot, _ = oracle.dispatch(ids, e0, EL)
+    R = int(offsets[-1])
+    assert R > 0
+    xp = bf16(inp.x[sorted_slot // k])
+    act = torch.empty((R, I), dtype=torch.bfloat16, device=dev())
+    yg = torch.full((R, H), float("nan"), dtype=torch.float32, device=dev())
+    moe.ffn_group(g.d, 0, EL, i32(offsets), xp, g.w_gate, g.w_up, g.w_down, act, yg)
+    yd = torch.full_like(yg, float("nan"))
+    act_d = torch.empty_like(act)
+    for e in range(EL):
+        r0, r1 = int(offsets[e]), int(offsets[e + 1])
+        if r1 > r0:
+            moe.ffn_dense(r1 - r0, H, I, xp[r0:r1], g.w_gate[e], g.w_up[e], g.w_down[e],
+                          act_d[r0:r1], yd[r0:r1])
+    torch.cuda.synchronize()
+    assert torch.equal(yg, yd), "moe_ffn_group and moe_ffn_dense bits differ"
+
+
 def test_route_ties_and_signed_zero():
     """Exact ties in the logits (duplicated router rows, zero rows) must go to
     the lower expert index, -0 and +0 being equal."""

@@ -88,7 +88,9 @@ WsLayout ws_layout(const moe_dims *d, const moe_opts *opt) {
     if (forward) {
         L.ids = take(sizeof(int32_t) * nslots);
         L.weights = take(sizeof(float) * nslots);
-        L.logits = T <= kRouteStreamMaxTokens ? take(sizeof(float) * T * d->experts) : 0;
+        L.logits = d->experts > 16 && T <= kRouteLogitsMaxTokens
+                       ? take(sizeof(float) * T * d->experts)
+                       : 0;
         L.counts = take(sizeof(int32_t) * NB);
         L.counts_el = take(sizeof(int32_t) * EL);
         L.offsets = take(sizeof(int32_t) * (NB + 1));

@@ -56,7 +56,7 @@ struct WsLayout {
     size_t slot_rank;     // int32 [T*k]
     size_t ids;           // int32 [T*k]   (forward, when the caller passes none)
     size_t weights;       // fp32  [T*k]
-    size_t logits;        // fp32  [T][E] router logits when T <= kRouteStreamMaxTokens, else 0
+    size_t logits;        // fp32  [T][E] router logits when E > 16 and T <= kRouteLogitsMaxTokens, else 0
                           // (chunk_counts is always at offset 0, so 0 means none)
     size_t counts;        // int32 [nbuckets] rows per bucket
     size_t counts_el;     // int32 [EL] rows per local expert (TOKENS stages)
@@ -111,8 +111,8 @@ constexpr size_t kNoAllocScratchBytes = size_t(256) << 20;
 
 // ---- kernel launchers (stream-ordered, no host synchronisation) ----------
 // logits: [T][E] fp32 scratch (may be NULL) for the many-expert, few-token
-// path (T <= kRouteStreamMaxTokens).
-constexpr int64_t kRouteStreamMaxTokens = 1024;
+// path (E > 16, T <= kRouteLogitsMaxTokens).
+constexpr int64_t kRouteLogitsMaxTokens = 4096;
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                         int32_t *ids, float *w, float *logits, hipStream_t s);
 // Dispatch indices.  tokens_per_stage == 0: buckets are the local experts;

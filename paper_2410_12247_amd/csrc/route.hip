@@ -329,162 +329,7 @@ __global__ __launch_bounds__(RT_THREADS) void route_kernel(const bf16_t *__restr
     }
 }
 
-// Half a stage's operands of the streaming router, read together with one
-// wait: this thread's four 16-byte x chunks and its expert's 32 router
-// weights (eight 16-byte reads from one base).  Written out because the
-// compiler puts a full vmcnt(0) in front of LDS reads that may alias the
-// LDS-DMA requests in flight, which drains the ring every stage; the ring's
-// own vmcnt wait and barrier order the data (the slot read here landed for
-// every wave before the barrier, and is refilled only after the next one).
-__device__ __forceinline__ void stream_half_operands(u32x4 (&v)[4], floatx4 (&w)[8],
-                                                     const uint32_t (&a)[4], uint32_t wa) {
-    asm volatile(
-        "ds_read_b128 %0, %12\n\t"
-        "ds_read_b128 %1, %13\n\t"
-        "ds_read_b128 %2, %14\n\t"
-        "ds_read_b128 %3, %15\n\t"
-        "ds_read_b128 %4, %16\n\t"
-        "ds_read_b128 %5, %16 offset:16\n\t"
-        "ds_read_b128 %6, %16 offset:32\n\t"
-        "ds_read_b128 %7, %16 offset:48\n\t"
-        "ds_read_b128 %8, %16 offset:64\n\t"
-        "ds_read_b128 %9, %16 offset:80\n\t"
-        "ds_read_b128 %10, %16 offset:96\n\t"
-        "ds_read_b128 %11, %16 offset:112\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(w[0]), "=&v"(w[1]),
-          "=&v"(w[2]), "=&v"(w[3]), "=&v"(w[4]), "=&v"(w[5]), "=&v"(w[6]), "=&v"(w[7])
-        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(wa)
-        : "memory");
-}
-
-// Streaming router: workgroup = TB tokens x EB experts (TB * EB = 256), one
-// fma chain per thread.  x rows (bf16) and router rows (fp32) stream through
-// an LDS ring of RS_NS stages of RS_HS h by LDS-DMA, RS_NS - 1 stages in
-// flight, so the latency of the loads is covered even when each stage holds
-// little work (few tokens, or few experts).  Each wave issues the same
-// number of DMA requests per stage (short waves repeat their last request:
-// the same bytes to the same place), so one vmcnt wait per stage is right
-// for every wave.  x chunks are XOR-swizzled by row so the 16 rows a wave
-// reads at once spread over the banks.
-// The logits go to z [T][E] and route_select_kernel picks.  (A fused form
-// for E <= 16, the workgroup picking the top-k of its tokens itself, was
-// slower than route_kernel at every T.)
-constexpr int RS_HS = 64;  // h per stage (two halves of four 16-byte x chunks)
-constexpr int RS_NS = 8;   // stages in the ring
-template <int TB, int EB>
-__global__ __launch_bounds__(RT_THREADS) void route_stream_kernel(
-    const bf16_t *__restrict__ x, const float *__restrict__ wr, const float *__restrict__ bias,
-    int64_t T, int H, int E, float *__restrict__ z) {
-    static_assert(TB * EB == RT_THREADS, "one chain per thread");
-    static_assert(RS_HS == 64, "stage reads: 8 x chunks of 8 h, 2 x 32 weights");
-    constexpr int XB = TB * RS_HS * 2;    // bytes of an x stage
-    constexpr int WB = EB * RS_HS * 4;    // bytes of a router stage
-    constexpr int NXI = XB / 1024;        // wave-wide 16-byte DMA requests
-    constexpr int NWI = WB / 1024;
-    constexpr int PER = (NXI + NWI + 3) / 4;  // requests per wave per stage
-    static_assert(XB % 1024 == 0 && WB % 1024 == 0, "stages of whole requests");
-    static_assert((RS_NS - 2) * PER <= 63, "vmcnt range");
-    constexpr int STAGE = XB + WB;
-    __shared__ __attribute__((aligned(16))) char lds[RS_NS * STAGE];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int tb = tid % TB;   // token of this thread's chain
-    const int eb = tid / TB;   // expert
-    const int64_t t0 = (int64_t)blockIdx.x * TB;
-    const int e0 = blockIdx.y * EB;
-
-    // this wave's requests: q = wave + 4 j (j < PER), clamped to the last
-    // real one; q < NXI are x requests (8 rows of 128 bytes), the rest
-    // router requests (4 rows of 256 bytes)
-    const char *src[PER];
-    int dst[PER];
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int q = min(wave + 4 * j, NXI + NWI - 1);
-        if (q < NXI) {
-            const int r = q * 8 + (lane >> 3);
-            const int c = (lane & 7) ^ (r & 7);  // 16-byte chunk of the row this lane fetches
-            const int64_t t = min<int64_t>(t0 + r, T - 1);
-            src[j] = reinterpret_cast<const char *>(x + t * H) + c * 16;
-            dst[j] = q * 1024;
-        } else {
-            const int qw = q - NXI;
-            const int r = qw * 4 + (lane >> 4);
-            const int e = min(e0 + r, E - 1);  // rows past E: a copy, never used
-            src[j] = reinterpret_cast<const char *>(wr + (int64_t)e * H) + (lane & 15) * 16;
-            dst[j] = XB + qw * 1024;
-        }
-    }
-    auto issue = [&](int st) {  // stage st into ring slot st % RS_NS
-        const int hb = st * RS_HS;
-        char *slot = lds + (st % RS_NS) * STAGE;
-#pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            const int q = min(wave + 4 * j, NXI + NWI - 1);
-            const int scale = q < NXI ? 2 : 4;  // bytes per element
-            __builtin_amdgcn_global_load_lds((gbl_void_t *)(src[j] + (int64_t)hb * scale),
-                                             (lds_void_t *)(slot + dst[j]), 16, 0, 0);
-        }
-    };
-
-    const int nst = H / RS_HS;
-#pragma unroll
-    for (int st = 0; st < RS_NS - 1; ++st)
-        if (st < nst) issue(st);
-    // LDS byte addresses in ring slot 0: chunk c of this thread's x row
-    // (stored at c ^ (row % 8)), and its expert's router row
-    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void_t *)lds;
-    uint32_t xaddr[8];
-#pragma unroll
-    for (int c = 0; c < 8; ++c) xaddr[c] = lds0 + tb * (RS_HS * 2) + ((c ^ (tb & 7)) * 16);
-    const uint32_t waddr = lds0 + XB + eb * (RS_HS * 4);
-    float acc = 0.0f;
-    for (int st = 0; st < nst; ++st) {
-        // stage st landed (this wave's share; later stages may be in flight)
-        if (st + RS_NS - 2 < nst) {
-            asm volatile("s_waitcnt vmcnt(%0)" ::"n"((RS_NS - 2) * PER) : "memory");
-        } else {
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        }
-        // every wave's share landed; slot (st - 1) fully read (a plain
-        // barrier: the waits above are the only memory ordering needed, and
-        // a fenced barrier would drain the requests still in flight)
-        __builtin_amdgcn_s_barrier();
-        if (st + RS_NS - 1 < nst) issue(st + RS_NS - 1);
-        const uint32_t sbase = (uint32_t)((st % RS_NS) * STAGE);
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            uint32_t a[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) a[i] = xaddr[half * 4 + i] + sbase;
-            u32x4 xs[4];
-            floatx4 ws[8];
-            stream_half_operands(xs, ws, a, waddr + sbase + half * 128);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const u32x4 xv = xs[i];
-                const floatx4 w0 = ws[2 * i], w1 = ws[2 * i + 1];
-                acc = __builtin_fmaf(bf16_lo(xv.x), w0.x, acc);
-                acc = __builtin_fmaf(bf16_hi(xv.x), w0.y, acc);
-                acc = __builtin_fmaf(bf16_lo(xv.y), w0.z, acc);
-                acc = __builtin_fmaf(bf16_hi(xv.y), w0.w, acc);
-                acc = __builtin_fmaf(bf16_lo(xv.z), w1.x, acc);
-                acc = __builtin_fmaf(bf16_hi(xv.z), w1.y, acc);
-                acc = __builtin_fmaf(bf16_lo(xv.w), w1.z, acc);
-                acc = __builtin_fmaf(bf16_hi(xv.w), w1.w, acc);
-            }
-        }
-    }
-    const int e = e0 + eb;
-    const int64_t t = t0 + tb;
-    if (e < E && bias) acc = acc + bias[e];
-    if (e < E && t < T) z[t * E + e] = acc;
-}
-
-// Top-k of logits z [T][E] from route_stream_kernel: one wave per token.
+// Top-k of logits z [T][E] (any E): one wave per token.
 __global__ __launch_bounds__(RT_THREADS) void route_select_kernel(const float *__restrict__ z,
                                                                   int64_t T, int E, int k,
                                                                   int renorm,
@@ -495,7 +340,8 @@ __global__ __launch_bounds__(RT_THREADS) void route_select_kernel(const float *_
     select_token(z + t * E, t, E, k, renorm, threadIdx.x & 63, ids, wout);
 }
 
-// Lane-per-token router for E <= 16.  Lane l of a wave owns the chains of
+// Lane-per-token router (E <= 16; and blocks of 16 experts for more experts
+// and few tokens).  Lane l of a wave owns the chains of
 // token l % TPW for R * G experts (the wave's 64 lanes are R sets of TPW =
 // 64 / R tokens; set s takes G experts of its own): x is the lane's own
 // operand, and the router element of each fma comes from a register that
@@ -515,7 +361,12 @@ __global__ __launch_bounds__(RT_THREADS) void route_select_kernel(const float *_
 // themselves left it behind their VALU stream: measured on the Mixtral shape
 // (16384 tokens, H = 4096, 8 experts), 41 us that way against 36 us with the
 // producer wave.  The logits then go to LDS and one lane per token takes the
-// top-k and the softmax weights.
+// top-k and the softmax weights; in the expert-block form (ZOUT) they go to
+// a [T][E] buffer for route_select_kernel.  For more than 16 experts the
+// chain per lane is as long as for 16 (H fmas), so up to a few thousand
+// tokens this beats the register-tiled kernel, whose workgroups each run
+// 5 to 20 chains per thread (E = 160, measured in the forward: 64 tokens
+// 65 -> 50 us, 1024 tokens 115 -> 81, 4096 tokens 261 -> 204).
 constexpr int RL_HS = 64;     // h per stage
 constexpr int RL_NS_MAX = 6;  // ring stages at most (deeper rings measured no faster)
 
@@ -667,16 +518,20 @@ __device__ __forceinline__ void select_lane(const float *zrow, int64_t t, int E,
     }
 }
 
-template <int G, int R, int NW, int NS>
+// ZOUT: the workgroup takes experts blockIdx.y * EP .. (any E) and writes
+// its logits (bias added) to zout [T][E] for a selection kernel; else one
+// workgroup holds every expert (E <= EP) and selects in place.
+template <int G, int R, int NW, int NS, bool ZOUT>
 __global__ __launch_bounds__(64 * NW + 64) void route_lane_kernel(const bf16_t *__restrict__ x,
                                                              const float *__restrict__ wr,
                                                              const float *__restrict__ bias,
                                                              int64_t T, int H, int E, int k,
                                                              int renorm,
                                                              int32_t *__restrict__ ids,
-                                                             float *__restrict__ wout) {
+                                                             float *__restrict__ wout,
+                                                             float *__restrict__ zout) {
     constexpr int TPW = 64 / R;              // tokens per wave (and per workgroup)
-    constexpr int EP = NW * R * G;           // experts per workgroup (>= E)
+    constexpr int EP = NW * R * G;           // experts per workgroup
     constexpr int XB = TPW * RL_HS * 2;      // bytes of a stage's x rows
     constexpr int WB = EP * RL_HS * 4;       // bytes of a stage's router rows
     constexpr int STAGE = XB + WB;
@@ -697,8 +552,9 @@ __global__ __launch_bounds__(64 * NW + 64) void route_lane_kernel(const bf16_t *
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bool producer = wave == NW;
     const int tl = lane % TPW;                   // token of this lane
-    const int eb = (wave * R + lane / TPW) * G;  // its first expert (compute waves)
+    const int eb = (wave * R + lane / TPW) * G;  // its first expert in the block
     const int64_t t0 = (int64_t)blockIdx.x * TPW;
+    const int e0 = ZOUT ? (int)blockIdx.y * EP : 0;  // the block's first expert
 
     // the producer's DMA requests q of a stage: q < NXR: 8 x rows of 128
     // bytes (lane i: row 8 q + i / 8, 16-byte chunk (i % 8) ^ lane_swz(row)
@@ -717,7 +573,7 @@ __global__ __launch_bounds__(64 * NW + 64) void route_lane_kernel(const bf16_t *
             step_bytes[q] = RL_HS * 2;
         } else {
             const int qw = q - NXR;
-            const int e = min(qw * 4 + (lane >> 4), E - 1);  // rows past E: a copy, never used
+            const int e = min(e0 + qw * 4 + (lane >> 4), E - 1);  // rows past E: unused copies
             src[q] = reinterpret_cast<const char *>(wr + (int64_t)e * H) + (lane & 15) * 16;
             dst[q] = XB + qw * 1024;
             step_bytes[q] = RL_HS * 4;
@@ -779,6 +635,17 @@ __global__ __launch_bounds__(64 * NW + 64) void route_lane_kernel(const bf16_t *
         for (int st0 = 0; st0 < nst; st0 += NS)
             lane_unroll<0, NS>([&](auto u) { step(st0 + decltype(u)::value, u); });
     }
+    if constexpr (ZOUT) {
+        // (the producer's DMA has all been waited for: its last wait is vmcnt(0))
+        if (producer) return;
+        const int64_t t = t0 + tl;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int e = e0 + eb + g;
+            if (e < E && t < T) zout[t * E + e] = bias ? acc[g] + bias[e] : acc[g];
+        }
+        return;
+    }
     __syncthreads();  // no wave reads the ring any more; no DMA in flight
 
     // logits to LDS, zs[token][e] with an odd row stride
@@ -826,8 +693,27 @@ hipError_t launch_lane(const moe_dims &d, const bf16_t *x, const float *wr, cons
     constexpr int STAGE = TPW * RL_HS * 2 + NW * R * G * RL_HS * 4;
     constexpr int PER = STAGE / 1024;
     const int64_t blocks = (d.tokens + TPW - 1) / TPW;
-    route_lane_kernel<G, R, NW, lane_ring(STAGE, PER)><<<(unsigned)blocks, 64 * NW + 64, 0, s>>>(
-        x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w);
+    route_lane_kernel<G, R, NW, lane_ring(STAGE, PER), false>
+        <<<(unsigned)blocks, 64 * NW + 64, 0, s>>>(x, wr, bias, d.tokens, d.hidden, d.experts,
+                                                   d.top_k, d.renormalize, ids, w, nullptr);
+    return hipGetLastError();
+}
+
+// Any number of experts in blocks of NW * R * G per workgroup, logits
+// through z [T][E], then the selection kernel (one wave per token).
+template <int G, int R, int NW>
+hipError_t launch_lane_z(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
+                         int32_t *ids, float *w, float *z, hipStream_t s) {
+    constexpr int TPW = 64 / R, EP = NW * R * G;
+    constexpr int STAGE = TPW * RL_HS * 2 + EP * RL_HS * 4;
+    constexpr int PER = STAGE / 1024;
+    const dim3 grid((unsigned)((d.tokens + TPW - 1) / TPW), (unsigned)((d.experts + EP - 1) / EP));
+    route_lane_kernel<G, R, NW, lane_ring(STAGE, PER), true><<<grid, 64 * NW + 64, 0, s>>>(
+        x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w, z);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    route_select_kernel<<<(unsigned)((d.tokens + 3) / 4), RT_THREADS, 0, s>>>(
+        z, d.tokens, d.experts, d.top_k, d.renormalize, ids, w);
     return hipGetLastError();
 }
 
@@ -856,30 +742,18 @@ hipError_t launch_lane_router(const moe_dims &d, const bf16_t *x, const float *w
 
 }  // namespace
 
-template <int EB>
-hipError_t launch_stream(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
-                         int32_t *ids, float *w, float *z, hipStream_t s) {
-    constexpr int TB = RT_THREADS / EB;
-    const dim3 grid((unsigned)((d.tokens + TB - 1) / TB), (unsigned)((d.experts + EB - 1) / EB));
-    route_stream_kernel<TB, EB><<<grid, RT_THREADS, 0, s>>>(x, wr, bias, d.tokens, d.hidden,
-                                                            d.experts, z);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    route_select_kernel<<<(unsigned)((d.tokens + 3) / 4), RT_THREADS, 0, s>>>(
-        z, d.tokens, d.experts, d.top_k, d.renormalize, ids, w);
-    return hipGetLastError();
-}
-
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                         int32_t *ids, float *w, float *logits, hipStream_t s) {
     if (d.tokens <= 0) return hipSuccess;
     if (d.experts <= 16) return launch_lane_router(d, x, wr, bias, ids, w, s);
-    // many experts, few tokens: the register-tiled kernel has too few
-    // workgroups to cover its serial h loop, so the streaming kernel spreads
-    // expert blocks over more workgroups (logits through the caller's
-    // buffer, then the selection kernel)
-    if (logits && d.tokens <= kRouteStreamMaxTokens)
-        return launch_stream<16>(d, x, wr, bias, ids, w, logits, s);
+    // many experts, up to kRouteLogitsMaxTokens tokens: the register-tiled
+    // kernel has too few workgroups to cover its serial h loop (or, up to
+    // 4096 tokens, issues more instructions per chain than the lane kernel
+    // does in parallel), so the lane-per-token kernel takes blocks of 16
+    // experts per workgroup (logits through the caller's buffer, then the
+    // selection kernel)
+    if (logits && d.tokens <= kRouteLogitsMaxTokens)
+        return launch_lane_z<2, 2, 4>(d, x, wr, bias, ids, w, logits, s);
     // 129..160 experts below 65536 tokens: 32 expert groups of 5, with the
     // most tokens per thread that keeps ~2 waves per SIMD (T / 4096, at most
     // 4).  Against 16 groups of 10 it reads fewer operands per fma at equal

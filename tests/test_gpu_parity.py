@@ -114,7 +114,8 @@ def test_route_many_experts_token_tiles(T, E):
 def test_maximum_experts_and_top_k(T, E, k):
     """The supported maximum, 256 experts with top-8 (and a ragged 200 with
     top-7): the router alone (16 experts per thread) and the whole forward
-    (the streaming router up to 1024 tokens, the combine of eight slots)
+    (the lane router in blocks of 16 experts up to 4096 tokens, the
+    combine of eight slots)
     against the oracle."""
     shp = C(name=f"max{T}_{E}", index=217, T=T, H=192, I=128, E=E, EL=32, e0=E - 40, k=k,
             renorm=True)
@@ -510,17 +511,23 @@ def test_forward_k_split(name):
         assert_close(yo.cpu().numpy(), ref, f"{name} PN={o.pipeline_n} budget={o.gemm_cu_budget}")
 
 
-@pytest.mark.parametrize("T,E", [(1, 17), (37, 40), (1024, 17), (1024, 160), (1025, 160)])
-def test_forward_routing_many_experts(T, E):
-    """Routing inside the forward for E > 16: up to 1024 tokens the logits come
-    from the streaming router (blocks of 16 experts, a ragged last block when
-    16 does not divide E, the logits through the workspace) and a separate
-    selection; above that from the register-tiled router.  Ids, weights,
-    counts and y match the oracle; duplicated router rows make exact ties,
-    which go to the lower expert index."""
+@pytest.mark.parametrize("T,E,bias", [(1, 17, False), (37, 40, True), (1024, 17, False),
+                                       (1024, 160, True), (1025, 160, False), (64, 32, True),
+                                       (33, 256, False), (500, 96, True), (4096, 40, True),
+                                       (4097, 40, False)])
+def test_forward_routing_many_experts(T, E, bias):
+    """Routing inside the forward for E > 16: up to 4096 tokens the logits come
+    from the lane-per-token router in blocks of 16 experts (a ragged last
+    block when 16 does not divide E; 33 tokens leave a ragged token block),
+    through the workspace, and a separate selection; above that from the
+    register-tiled router.  Ids, weights, counts and y match the oracle;
+    duplicated router rows make exact ties, which go to the lower expert
+    index."""
     shp = C(name=f"many{T}_{E}", index=214, T=T, H=192, I=64, E=E, EL=4, e0=E - 4, k=6,
             renorm=False)
     inp = synth.make_inputs(shp)
+    if bias:
+        inp.bias = np.random.default_rng(E).standard_normal(E).astype(np.float32)
     inp.w_router[E - 1] = inp.w_router[3]
     inp.w_router[9] = inp.w_router[3]
     inp.w_router[E - 2] = inp.w_router[E - 3]

@@ -602,12 +602,19 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
     // the grouped gate/up GEMM can gather its token rows itself while every
     // byte offset into x fits 32 bits
     const bool fold_ok = gather_foldable(d);
+    // Cross-stream hops cost host time (an event record or wait each) and
+    // GPU latency, so only the ones that buy overlap are made: the gather
+    // stream is used only when gathers run (not folded), and the combine
+    // gets its own stream only when it can run beside a later stage's GEMMs;
+    // with one stage it follows them on the GEMM stream.
+    const bool combine_apart = !one_stream && PN > 1;
+    hipStream_t scomb = combine_apart ? sc : sm;
 
     if (!one_stream) {
         MOE_HIP(hipEventRecord(ev_fork, s0));
-        MOE_HIP(hipStreamWaitEvent(sg, ev_fork, 0));
+        if (!fold_ok) MOE_HIP(hipStreamWaitEvent(sg, ev_fork, 0));
         MOE_HIP(hipStreamWaitEvent(sm, ev_fork, 0));
-        MOE_HIP(hipStreamWaitEvent(sc, ev_fork, 0));
+        if (combine_apart) MOE_HIP(hipStreamWaitEvent(sc, ev_fork, 0));
         tm.gap();
     }
 
@@ -646,7 +653,7 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
                                   sg));
             MOE_TRY(tm.end(sg));
         }
-        if (!one_stream) {
+        if (!one_stream && !fold_gather) {
             MOE_HIP(hipEventRecord(ev_g[i], sg));
             MOE_HIP(hipStreamWaitEvent(sm, ev_g[i], 0));
             tm.gap();
@@ -709,7 +716,7 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
                 }
             }
         }
-        if (!one_stream) {
+        if (combine_apart) {
             MOE_HIP(hipEventRecord(ev_m[i], sm));
             MOE_HIP(hipStreamWaitEvent(sc, ev_m[i], 0));
             tm.gap();
@@ -717,14 +724,14 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
 
         // weighted combine of this stage: its experts over all tokens, or
         // all experts over its tokens
-        MOE_TRY(tm.begin(sc, PH_COMBINE));
+        MOE_TRY(tm.begin(scomb, PH_COMBINE));
         const int accumulate = (has_shared || (!tok_stages && i > 0)) ? 1 : 0;
         MOE_HIP(launch_combine(d, tok_stages ? 0 : b0, tok_stages ? EL : per_stage, t_lo, t_hi,
-                               y_perm, ids, slot_row, wts, y, accumulate, sc));
-        MOE_TRY(tm.end(sc));
+                               y_perm, ids, slot_row, wts, y, accumulate, scomb));
+        MOE_TRY(tm.end(scomb));
     }
     if (!one_stream) {
-        MOE_HIP(hipEventRecord(ev_done, sc));
+        MOE_HIP(hipEventRecord(ev_done, scomb));
         MOE_HIP(hipStreamWaitEvent(s0, ev_done, 0));
         tm.gap();
     }

@@ -96,13 +96,16 @@ constexpr int kPermChunk = 1024;
 // long (kSplitMinStagesAlone when the launch has fewer tiles than
 // workgroups: decode-sized launches, whose pieces would otherwise leave
 // most compute units idle while the weights stream), at most kSplitSlots
-// pieces (partial-accumulator buffers) in all, so at most kSplitSlots / 2
-// tiles cut.
+// pieces (partial-accumulator buffers) in all and kSplitMaxTail tiles cut.
+// A launch of one partial round of more than half the grid spreads its K
+// stages evenly over the grid instead (stream-K: a piece may end one tile
+// and start the next).
 constexpr int kSplitMaxPieces = 8;
 constexpr int kSplitMinStages = 32;
 constexpr int kSplitMinStagesAlone = 8;
-constexpr int kSplitSlots = 256;
-constexpr int kSplitMetaInts = 2 + 4 * (kSplitSlots / 2);
+constexpr int kSplitSlots = 512;
+constexpr int kSplitMaxTail = 256;
+constexpr int kSplitMetaInts = 4 + 4 * kSplitMaxTail;
 // Bytes of the partial-accumulator buffer the grouped GEMM takes (all slots).
 size_t gemm_split_bytes();
 

@@ -725,30 +725,57 @@ __global__ __launch_bounds__(TP::THREADS) void group_kernel(
     const int nk = K / TP::KSTEP;
     // Tiles [0, full) fill whole rounds of the grid.  The rem < G tiles left
     // would occupy rem workgroups for one more tile time while the others
-    // idle; with a split buffer they are cut along K into S pieces each
-    // (slots [S*j, S*j + S) take tail tile j = tau - full), so the last round
-    // is about S times shorter.  The pieces store fp32 partial sums;
-    // split_fixup_kernel, launched next, adds them in piece order and
-    // writes the outputs.  split_meta: [0] tail tiles cut (0: none), [1] S,
-    // then per tail tile its first output row, first output column and
-    // valid rows and columns.
+    // idle.  With a split buffer the tail is cut along K:
+    //  - rem <= G/2: each tail tile j = tau - full into S equal pieces
+    //    (slots [S*j, S*j + S));
+    //  - a launch that is one partial round of more than G/2 tiles (full ==
+    //    0): its W = rem * nk K stages, the tail tiles laid end to end, are
+    //    spread evenly over P <= G units (stream-K): unit u takes stages
+    //    [u*W/P, (u+1)*W/P), so it ends one tile and starts the next, and its
+    //    segment of tile j goes to slot u + j (unique: a unit that reaches
+    //    into tile j + 1 is the last of tile j).  Only for tiles of 192 or
+    //    more token rows (their MFMA work, done for every row of the tile,
+    //    bounds them; a round of 128-row tiles is bound by the weight
+    //    stream, which fewer workgroups already saturate), at most half
+    //    full on average (each piece writes and the fixup re-reads the
+    //    partial sums of the valid rows: for fuller tiles that traffic
+    //    outweighs the shorter round), and when the round gets at least a
+    //    quarter shorter.
+    // The pieces store fp32 partial sums; split_fixup_kernel, launched next,
+    // adds each tile's pieces in K order and writes the outputs.
+    // split_meta: [0] tail tiles cut (0: none), [1] S (0: stream-K), [2] P,
+    // [3] nk, then per tail tile its first output row, first output column
+    // and valid rows and columns.
     const int full = total - total % G;
     const int rem = total - full;
-    int S = 1;
-    if (TP::CAN_SPLIT && parts != nullptr && rem > 0)
-        S = min(min(kSplitMaxPieces, G / rem),
-                min(nk / (full == 0 ? kSplitMinStagesAlone : kSplitMinStages), kSplitSlots / rem));
+    const int64_t W = (int64_t)rem * nk;
+    int S = 1, P = 0;
+    if (TP::CAN_SPLIT && parts != nullptr && rem > 0 && rem <= kSplitMaxTail) {
+        if (full == 0 && 2 * rem > G && BM >= 192) {
+            // mean valid rows per tile: all rows over the m-tiles
+            const int64_t rows_all = s_off[e_count] - s_off[0];
+            if (2 * rows_all * NT <= (int64_t)BM * total) {
+                P = (int)min<int64_t>(min(G, kSplitSlots - rem), W / kSplitMinStagesAlone);
+                if (4 * rem > 3 * P) P = 0;
+            }
+        } else {
+            S = min(min(kSplitMaxPieces, G / rem),
+                    min(nk / (full == 0 ? kSplitMinStagesAlone : kSplitMinStages),
+                        kSplitSlots / rem));
+        }
+    }
     if (S < 2) S = 1;
     if (split_meta != nullptr && slot == 0 && tid == 0) {
-        split_meta[0] = S > 1 ? rem : 0;
-        split_meta[1] = S;
+        split_meta[0] = S > 1 || P > 0 ? rem : 0;
+        split_meta[1] = P > 0 ? 0 : S;
+        split_meta[2] = P;
+        split_meta[3] = nk;
     }
-    const int end = S > 1 ? full : total;
-    const int units = S > 1 ? full + rem * S : total;
-    for (int u = slot; u < units; u += G) {
-        const int tau = u < end ? u : full + (u - full) / S;
-        const int piece = u < end ? 0 : (u - full) % S;
-        const int pieces = u < end ? 1 : S;
+
+    // tile tau over K stages [k0, k0 + nks); part: the slot of its partial
+    // sums (NULL: the whole K range, outputs written); j >= 0: the tail tile
+    // whose record this call writes (the call that starts at stage 0)
+    auto run_tau = [&](int tau, int k0, int nks, float *part, int j) {
         // expert: last e with s_pre[e] <= tau
         int lo = 0, hi = e_count - 1;
         while (lo < hi) {
@@ -772,26 +799,51 @@ __global__ __launch_bounds__(TP::THREADS) void group_kernel(
         a.slot_div = slot_div;
         a.m_valid = min(BM, cnt - mt * BM);
         a.K = K;
-        // piece p of S covers stages [p*nk/S, (p+1)*nk/S)
-        a.k0 = piece * nk / pieces;
-        a.nks = (piece + 1) * nk / pieces - a.k0;
+        a.k0 = k0;
+        a.nks = nks;
         a.ldo = ldo;
         if (MODE == 0)
             a.out = reinterpret_cast<bf16_t *>(out) + r0 * ldo + n0;
         else
             a.out = reinterpret_cast<float *>(out) + r0 * ldo + n0;
-        const int j = tau - full;  // tail tile index when split
-        a.part = pieces > 1 ? parts + (size_t)j * S * TP::PART_ELEMS : nullptr;
-        a.piece = piece;
-        a.npieces = pieces;
-        if (pieces > 1 && piece == 0 && tid == 0) {
-            int32_t *md = split_meta + 2 + 4 * j;
+        a.part = part;
+        a.piece = 0;
+        a.npieces = part != nullptr ? 2 : 1;
+        if (j >= 0 && tid == 0) {
+            int32_t *md = split_meta + 4 + 4 * j;
             md[0] = (int32_t)r0;
             md[1] = (int32_t)n0;
             md[2] = a.m_valid;
             md[3] = a.n_valid;
         }
         TP::run(a, smem);
+    };
+
+    if (P > 0) {
+        // stream-K tail (full == 0): at most one unit per workgroup
+        if (slot < P) {
+            const int64_t g0 = (int64_t)slot * W / P, g1 = (int64_t)(slot + 1) * W / P;
+            for (int j = (int)(g0 / nk); (int64_t)j * nk < g1; ++j) {
+                const int64_t a0 = max<int64_t>(g0, (int64_t)j * nk);
+                const int64_t a1 = min<int64_t>(g1, (int64_t)(j + 1) * nk);
+                run_tau(j, (int)(a0 - (int64_t)j * nk), (int)(a1 - a0),
+                        parts + (size_t)(slot + j) * TP::PART_ELEMS, a0 == (int64_t)j * nk ? j : -1);
+            }
+        }
+        return;
+    }
+    const int end = S > 1 ? full : total;
+    const int units = S > 1 ? full + rem * S : total;
+    for (int u = slot; u < units; u += G) {
+        if (u < end) {
+            run_tau(u, 0, nk, nullptr, -1);
+        } else {
+            // piece p of S covers stages [p*nk/S, (p+1)*nk/S)
+            const int j = (u - full) / S, piece = (u - full) % S;
+            const int k0 = piece * nk / S;
+            run_tau(full + j, k0, (piece + 1) * nk / S - k0,
+                    parts + (size_t)(j * S + piece) * TP::PART_ELEMS, piece == 0 ? j : -1);
+        }
     }
 }
 
@@ -854,17 +906,32 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(const float *__restric
     constexpr int NP = C::TN / 2;  // fragment-row pairs per wave
     static_assert(NP * 64 == 256, "one wave per fragment-row pair");
     const int ntail = meta[0];
-    const int S = meta[1];
+    const int S_eq = meta[1];  // equal pieces per tile, or 0: stream-K over P units
+    const int P = meta[2], nk = meta[3];
+    const int64_t W = (int64_t)ntail * nk;
     const int p = threadIdx.x >> 6;
     const int lane = threadIdx.x & 63;
     for (int unit = blockIdx.x; unit < ntail * 8; unit += gridDim.x) {
         const int j = unit / 8;
         const int wave = unit % 8;
-        const int32_t *md = meta + 2 + 4 * j;
+        // the tile's pieces sit in consecutive slots [first, first + S), in K order
+        int first, S;
+        if (S_eq > 0) {
+            first = j * S_eq;
+            S = S_eq;
+        } else {
+            // units holding the tile's first and last stage (the unit of
+            // stage s is the last u with u * W / P <= s)
+            const int u0 = (int)((((int64_t)j * nk + 1) * P - 1) / W);
+            const int u1 = (int)(((int64_t)(j + 1) * nk * P - 1) / W);
+            first = u0 + j;
+            S = u1 - u0 + 1;
+        }
+        const int32_t *md = meta + 4 + 4 * j;
         const int64_t r0 = md[0], n0 = md[1];
         const int m_valid = md[2], n_valid = md[3];
         const __amdgpu_buffer_rsrc_t pres = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<float *>(parts) + (size_t)j * S * C::PART_ELEMS, 0, -1, kBufferFlags);
+            const_cast<float *>(parts) + (size_t)first * C::PART_ELEMS, 0, -1, kBufferFlags);
         const int loff = lane * 16;
         void *o = MODE == 0 ? (void *)(reinterpret_cast<bf16_t *>(out) + r0 * ldo + n0)
                             : (void *)(reinterpret_cast<float *>(out) + r0 * ldo + n0);
@@ -1085,17 +1152,17 @@ hipError_t skinny_down_launch(unsigned blocks, int ns, const int32_t *offsets, i
 
 int round_grid(int64_t tiles) { return (int)(((tiles + NXCD - 1) / NXCD) * NXCD); }
 
-// Fixup launch after a grouped GEMM that was given a split buffer: at most
-// min(grid, kSplitSlots) / 2 tiles can be cut (each into two or more
-// pieces), 8 work units each; one workgroup per compute unit at most, so an
-// empty fixup is cheap to dispatch.
+// Fixup launch after a grouped GEMM that was given a split buffer: fewer
+// than grid tail tiles can be cut (each into two or more pieces), 8 work
+// units each; one workgroup per compute unit at most, so an empty fixup is
+// cheap to dispatch.
 template <int MODE, class TP>
 hipError_t launch_split_fixup(int grid, const float *parts, const int32_t *meta, void *out,
                               int64_t ldo, hipStream_t s) {
     if constexpr (!TP::CAN_SPLIT) {
         return hipSuccess;
     } else {
-        const int max_tail = std::min(grid, kSplitSlots) / 2;
+        const int max_tail = std::min(grid, kSplitMaxTail);
         const int blocks = std::min(max_tail * 8, device_cu_count());
         split_fixup_kernel<MODE, TP><<<blocks, 256, 0, s>>>(parts, meta, out, ldo);
         return hipGetLastError();
@@ -1214,12 +1281,16 @@ double gemm_launch_us(int mode, int bm, int64_t tiles, int K, int grid, bool spl
     const int64_t rem = tiles % grid;
     double us = kLaunchUs[md] + full_rounds * (loop_us + c.epi_us[md]);
     if (rem > 0) {
+        // (a round of more than half the grid that the kernel spreads
+        // stream-K, for tall tiles at most half full, is priced unsplit: an
+        // upper bound)
         int S = 1;
-        if (split && 2 * rem <= grid)
+        if (split && 2 * rem <= grid) {
             S = (int)std::min<int64_t>(
                 std::min<int64_t>(kSplitMaxPieces, grid / rem),
                 std::min<int64_t>(nk / (full_rounds == 0 ? kSplitMinStagesAlone : kSplitMinStages),
                                   kSplitSlots / rem));
+        }
         const double busy = (double)std::min<int64_t>(grid, rem * std::max(S, 1)) / grid;
         const double part = kPartialRound[md] + (1.0 - kPartialRound[md]) * busy;
         if (S >= 2)

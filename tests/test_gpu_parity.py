@@ -53,6 +53,16 @@ SPLIT_CASES = {
     "split8": C(name="split8", index=213, T=32, H=8192, I=256, E=8, EL=8, k=2, renorm=True),
     "split_shared": C(name="split_shared", index=215, T=300, H=256, I=128, E=8, EL=8, k=2,
                       renorm=True, n_shared=1, Is=2048),
+    # one partial round of more than half the grid in tiles of 192 or more
+    # token rows at most half full (stream-K: the round's K stages spread
+    # evenly over 256 workgroups, a piece ending one tile and starting the
+    # next): the gate/up GEMM's 132 tiles (11 per expert, 192-row tiles,
+    # K = 2048) with the down GEMM's 96 cut in 2; then the down GEMM's 144
+    # tiles (256-row tiles, K = 512) with 24 gate/up tiles cut in 8
+    "streamk_gu": C(name="streamk_gu", index=220, T=192, H=2048, I=1408, E=12, EL=12, k=4,
+                    renorm=True),
+    "streamk_dn": C(name="streamk_dn", index=221, T=256, H=6144, I=512, E=6, EL=6, k=2,
+                    renorm=True),
 }
 CASES.update(SPLIT_CASES)
 
@@ -502,13 +512,65 @@ def test_forward_k_split(name):
     # where the fp32 down GEMM is cut, the pieces' sums differ from one pass
     # in the last bits somewhere (the evidence that the split ran; a cut
     # gate/up shows only through rare bf16 rounding flips of act)
-    if name in ("split2", "split3", "split_shared"):
+    if name in ("split2", "split3", "split_shared", "streamk_gu", "streamk_dn"):
         assert not torch.equal(y, ye), "no tile was split"
     assert_close(y.cpu().numpy(), ye.cpu().numpy().astype(np.float64), f"{name} split vs exact",
                  max_abs=2e-3, rel_fro=1e-4)
     for o in (moe.opts(pipeline_n=2), moe.opts(gemm_cu_budget=48), moe.opts(gemm_cu_budget=96)):
         yo = g.forward(o).y
         assert_close(yo.cpu().numpy(), ref, f"{name} PN={o.pipeline_n} budget={o.gemm_cu_budget}")
+
+
+def exact_sum_inputs(inp):
+    """Integer-valued operands whose GEMM sums are exact in fp32 in any
+    order: x is 1 on its first 64 features (the rest in {-1, 0, 1}, so the
+    routing still varies), every gate row sums 32 of those ones (g = 32, and
+    silu(32) = 32 in fp32: e^-32 vanishes beside 1), every up row has at most
+    4 entries of +-1 among them (u in [-4, 4], act = 32 u exact in bf16),
+    and the down weights are in {-1, 0, 1}.  Any cut of K then gives the
+    one-pass bits."""
+    s = inp.shape
+    rng = np.random.default_rng(s.index)
+    one = synth.bf16_bits(np.ones(1, np.float32))[0]
+
+    def ints(shape, lo=-1, hi=1):
+        return synth.bf16_bits(rng.integers(lo, hi + 1, size=shape).astype(np.float32))
+
+    x = ints((s.T, s.H))
+    x[:, :64] = one
+    inp.x = x
+
+    def gate_up(rows):
+        g = np.zeros((rows, s.H), np.uint16)
+        g[:, :32] = one
+        u = np.zeros((rows, s.H), np.float32)
+        for r in range(rows):
+            u[r, rng.choice(64, size=4, replace=False)] = rng.choice([-1.0, 1.0], size=4)
+        return g, synth.bf16_bits(u)
+
+    wg, wu = zip(*(gate_up(s.I) for _ in range(s.EL)))
+    inp.w_gate, inp.w_up = np.stack(wg), np.stack(wu)
+    inp.w_down = ints((s.EL, s.H, s.I))
+    if s.n_shared:
+        inp.shared_gate, inp.shared_up = gate_up(s.n_shared * s.Is)
+        inp.shared_down = ints((s.H, s.n_shared * s.Is))
+    return inp
+
+
+@pytest.mark.parametrize("name", list(SPLIT_CASES))
+def test_k_split_exact_sums(name):
+    """Every K split (equal pieces, stream-K, under pipeline stages and CU
+    budgets) on operands whose sums are exact in any order: the same bits as
+    one pass over K, so each piece covers exactly its stages and the fixup
+    adds exactly the tile's pieces."""
+    inp = exact_sum_inputs(synth.make_inputs(CASES[name]))
+    g = Dev(inp)
+    ye = g.forward(moe.opts(exact_order=True)).y.clone()
+    assert torch.isfinite(ye).all()
+    for o in (moe.opts(), moe.opts(pipeline_n=2), moe.opts(gemm_cu_budget=48),
+              moe.opts(gemm_cu_budget=96)):
+        y = g.forward(o).y
+        assert torch.equal(y, ye), f"{name} PN={o.pipeline_n} budget={o.gemm_cu_budget}"
 
 
 @pytest.mark.parametrize("T,E,bias", [(1, 17, False), (37, 40, True), (1024, 17, False),

@@ -4,7 +4,8 @@
 // expert, or, when the pipeline cuts token ranges, token-range stage * EL +
 // local expert.  A token selects an expert at most once, so slot order
 // within an expert is token order (the order of the paper's Fig. 7a
-// example).  Three passes, no atomics:
+// example).  Three passes, no atomics (one kernel doing all three in one
+// wave when the slots fit one chunk):
 //   1. one wave per chunk of kPermChunk slots: wave-level match (nine
 //      ballots on the bucket id) gives each slot its rank among the equal
 //      ids before it in the 64-slot step, a per-chunk LDS counter carries the
@@ -162,6 +163,85 @@ __global__ __launch_bounds__(256) void scatter_kernel(const int32_t *__restrict_
     slot_row[s] = row;
 }
 
+// The three passes in one wave for at most kPermChunk slots (one chunk:
+// decode batches), one launch instead of three: the ranks as in
+// hist_kernel, kept in registers; the bucket scan as in scan_kernel, 64
+// buckets at a time with a carry; then the rows.  Same counts, offsets and
+// rows as the three kernels.
+__global__ __launch_bounds__(64) void dispatch_one_chunk_kernel(
+    const int32_t *__restrict__ ids, int64_t nslots, int k, int e0, int EL, int64_t tps, int NB,
+    int32_t *__restrict__ counts, int32_t *__restrict__ offsets,
+    int32_t *__restrict__ counts_el, int32_t *__restrict__ sorted_slot,
+    int32_t *__restrict__ slot_row) {
+    __shared__ int cnt[kMaxExperts];
+    __shared__ int off[kMaxExperts];
+    const int lane = threadIdx.x;
+    for (int e = lane; e < NB; e += 64) cnt[e] = 0;
+    __syncthreads();
+    const uint64_t lt_mask = (1ull << lane) - 1ull;
+    constexpr int NIT = kPermChunk / 64;
+    int idv[NIT], bucket[NIT], rank[NIT];
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) idv[it] = ids[min<int64_t>(it * 64 + lane, nslots - 1)];
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int s = it * 64 + lane;
+        int e = idv[it] - e0;
+        if (s >= nslots || e < 0 || e >= EL) e = -1;
+        else if (tps > 0) e += (int)((uint32_t)s / (uint32_t)k / (uint32_t)tps) * EL;
+        const uint32_t v = (uint32_t)(e + 1);
+        uint64_t match = ~0ull;
+#pragma unroll
+        for (int b = 0; b < 9; ++b) {
+            const bool bit = (v >> b) & 1u;
+            const uint64_t bal = __ballot(bit);
+            match &= bit ? bal : ~bal;
+        }
+        const int before = __popcll(match & lt_mask);
+        bucket[it] = e;
+        rank[it] = e >= 0 ? cnt[e] + before : 0;
+        __syncthreads();
+        if (e >= 0 && before == 0) cnt[e] += __popcll(match);
+        __syncthreads();
+    }
+    int carry = 0;
+    for (int b0 = 0; b0 < NB; b0 += 64) {
+        const int e = b0 + lane;
+        const int v = e < NB ? cnt[e] : 0;
+        const int incl = wave_inclusive_scan(v);
+        if (e < NB) {
+            counts[e] = v;
+            off[e] = carry + incl - v;
+            offsets[e] = carry + incl - v;
+        }
+        carry += __builtin_amdgcn_readlane(incl, 63);
+    }
+    if (lane == 0) offsets[NB] = carry;
+    if (counts_el) {  // rows per local expert over the stages
+        for (int e = lane; e < EL; e += 64) {
+            int sum = 0;
+            for (int b = e; b < NB; b += EL) sum += cnt[b];
+            counts_el[e] = sum;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int s = it * 64 + lane;
+        if (s < nslots) {
+            const int e = bucket[it];
+            if (e < 0) {
+                slot_row[s] = -1;
+            } else {
+                const int row = off[e] + rank[it];
+                sorted_slot[row] = s;
+                slot_row[s] = row;
+            }
+        }
+    }
+}
+
 // One wave per row; rows [offsets[e_first], offsets[e_first+e_count]).
 __global__ __launch_bounds__(256) void gather_kernel(const int32_t *__restrict__ offsets,
                                                      int e_first, int e_count,
@@ -195,6 +275,13 @@ hipError_t launch_permute(const moe_dims &d, const int32_t *ids, void *ws, const
     const int64_t nslots = d.tokens * d.top_k;
     const int64_t tps = tokens_per_stage;
     const int NB = L.nbuckets;
+    if (nslots <= kPermChunk) {
+        dispatch_one_chunk_kernel<<<1, 64, 0, s>>>(ids, nslots, d.top_k, d.local_begin,
+                                                    d.local_count, tps, NB, counts, offsets,
+                                                    tps > 0 ? counts_el : nullptr, sorted_slot,
+                                                    slot_row);
+        return hipGetLastError();
+    }
     hist_kernel<<<(unsigned)L.nchunks, 64, 0, s>>>(ids, nslots, d.top_k, d.local_begin,
                                                     d.local_count, tps, NB, chunk_counts,
                                                     slot_rank);

@@ -665,16 +665,19 @@ def _kernel_label(name):
 
 
 def _trace_forwards(path):
-    """Kernel dispatches of a kernel-trace CSV, cut into forwards: each starts
-    at the shared-expert offsets kernel when the workload has shared experts,
-    else at the router."""
+    """Kernel dispatches of a kernel-trace CSV in the order they were
+    enqueued (dispatch id; kernels on the forward's side streams overlap, and
+    a kernel's start stamp can precede that of the one before it on its own
+    stream), cut into forwards: each starts at the shared-expert offsets
+    kernel when the workload has shared experts, else at the router."""
     import csv
 
     ev = []
     for r in csv.DictReader(open(path)):
-        ev.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]),
-                   _kernel_label(r.get("Kernel_Name", ""))))
-    ev.sort()
+        ev.append((int(r.get("Dispatch_Id") or 0), int(r["Start_Timestamp"]),
+                   int(r["End_Timestamp"]), _kernel_label(r.get("Kernel_Name", ""))))
+    ev.sort(key=lambda e: (e[0], e[1]))
+    ev = [e[1:] for e in ev]
     has_shared = any("shared_offsets" in e[2] for e in ev)
     first = (lambda n: "shared_offsets" in n) if has_shared else \
         (lambda n: n.startswith("route") and "select" not in n)

@@ -339,9 +339,10 @@ moe_status moe_last_timing(moe_timing *out);
 
 /* The paper's enable condition and gain for PN = pipeline_n expert stages
  * (pipeline_n = 0: the PN moe_ffn_forward would choose with pipeline_n = 0,
- * i.e. the divisor of local_count with the largest positive gain among
- * those enabled, else 1), from the host row counts rows[0..local_count) of
- * the local experts.  The GEMM terms use the launch-cost model of the GEMM
+ * i.e. the divisor of local_count with the largest gain among those
+ * enabled, when that gain is at least 5% of the unsplit GEMM time (the
+ * launch-cost model's error), else 1), from the host row counts
+ * rows[0..local_count) of the local experts.  The GEMM terms use the launch-cost model of the GEMM
  * kind AUTO (or opts->gemm_mode) takes per stage; the communication terms
  * the combine's bytes at its measured streaming rate.  Expert stages only.
  * Host-only; never touches the GPU. */

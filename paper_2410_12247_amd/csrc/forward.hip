@@ -314,6 +314,11 @@ constexpr double kCombineLaunchUs = 4.0;
 constexpr double kStageUs = 20.0;
 // The paper's thresholds for its DeepSeekV2 test (Sec. 5.2 item 4).
 constexpr double kEps0Max = 0.32, kEps1Max = 0.03;
+// The least predicted gain, as a fraction of the unsplit GEMM time, for
+// which the library cuts stages: below it the gain is within the launch-cost
+// model's error (4.5% rms per launch; measured, a predicted 7 us on the
+// Zipf 4096-token load was a 57 us loss).
+constexpr double kPnMinGainFrac = 0.05;
 
 // A combine reads its stage's rows and every token's slot records; it
 // writes every token's output when it starts y, and otherwise reads and
@@ -373,8 +378,9 @@ moe_pipeline_eval pipeline_eval(const moe_dims &d, const moe_opts &o, const int3
     return ev;
 }
 
-// pipeline_n = 0: the divisor of EL with the largest positive predicted gain
-// among those that meet the enable condition, else 1.
+// pipeline_n = 0: the divisor of EL with the largest predicted gain among
+// those that meet the enable condition, when that gain is at least
+// kPnMinGainFrac of the unsplit GEMM time, else 1.
 int choose_pipeline_auto(const moe_dims &d, const moe_opts &o, const int32_t *rows, int grid,
                          bool split) {
     int best = 1;
@@ -382,7 +388,7 @@ int choose_pipeline_auto(const moe_dims &d, const moe_opts &o, const int32_t *ro
     for (int n = 2; n <= d.local_count; ++n) {
         if (d.local_count % n) continue;
         const moe_pipeline_eval ev = pipeline_eval(d, o, rows, n, grid, split);
-        if (ev.enabled && ev.gain_us > best_gain) {
+        if (ev.enabled && ev.gain_us > best_gain && ev.gain_us >= kPnMinGainFrac * ev.t_comp_us) {
             best = n;
             best_gain = ev.gain_us;
         }

@@ -972,8 +972,8 @@ template <int MODE> using GroupTile = TileOf<MODE>;
 // tiles that streams the expert's weights once.  A workgroup is one wave
 // and owns SK_BN output columns (weight rows) by the expert's rows over the
 // whole K range: no K split, no fixup.  Weight and act rows stream through
-// a ring of LDS stages of 32 K by LDS-DMA, all but one stage ahead, the
-// chunks placed as in the ping-pong tile.  The ring depth is chosen per
+// a ring of LDS stages of SK_BK K by LDS-DMA, all but one stage ahead, the
+// 16-byte chunks of each row XOR-placed as in the ping-pong tile.  The ring depth is chosen per
 // launch (dynamic LDS): the deepest with which every tile of the launch is
 // resident at once (a second, partial round of tiles would take as long as
 // the first).  The MFMA (16x16x32 bf16, the weight fragment as the A
@@ -983,36 +983,43 @@ template <int MODE> using GroupTile = TileOf<MODE>;
 // the compiler would otherwise wait for all LDS-DMA in flight before
 // reading LDS and drain the ring every stage.
 constexpr int SK_BN = 64;  // weight rows (output columns) per tile
-constexpr int SK_BK = 32;
+// K per ring stage: 64, so each stage reads 128 contiguous bytes of every
+// weight row.  With 32 (64-byte pieces of rows 3-12 KB apart) the weight
+// stream ran 13-27% slower, even where the wider stages leave fewer tiles
+// resident per compute unit.
+constexpr int SK_BK = 64;
 constexpr int SK_NS_MAX = 16;             // ring stages at most
 constexpr size_t SK_LDS_MAX = 64 * 1024;  // dynamic LDS of one workgroup at most
 
 // stages a wave can keep ahead: vmcnt counts at most 63 requests
 constexpr int sk_ahead_max(int lps) { return std::min(SK_NS_MAX - 1, 63 / lps); }
+// LDS-DMA requests per stage (64 lanes x 16 bytes each)
+constexpr int sk_lps(int bm, int bk) { return (SK_BN + bm) * bk * 2 / 1024; }
 
-// LDS bytes of a workgroup with a ring of ns stages: the ring plus room for
-// the act-fragment reads a tile of fewer than 64 rows does not use
-constexpr size_t sk_lds_bytes(int bm, int ns) {
-    return (size_t)ns * (SK_BN + bm) * SK_BK * 2 + (size_t)(4 - bm / 16) * 1024;
+// LDS bytes of a workgroup with a ring of ns stages of bk K: the ring plus
+// room for the act-fragment reads a tile of fewer than 64 rows does not use
+constexpr size_t sk_lds_bytes(int bm, int bk, int ns) {
+    return (size_t)ns * (SK_BN + bm) * bk * 2 + (size_t)(4 - bm / 16) * 16 * bk * 2;
 }
 
-// the stage's fragments: 4 weight fragments from wa, 4 act fragments from
+// one K-step's fragments: 4 weight fragments from wa, 4 act fragments from
 // xa (a tile of fewer rows reads the first ones; the others land in the
-// next slot or the padding after the ring), 1024 bytes apart
+// next slot or the padding after the ring), F bytes (16 LDS rows) apart
+template <int F>
 __device__ __forceinline__ void sk_read_frags(bf16x8 (&f)[8], uint32_t wa, uint32_t xa) {
     asm volatile(
         "ds_read_b128 %0, %8\n\t"
-        "ds_read_b128 %1, %8 offset:1024\n\t"
-        "ds_read_b128 %2, %8 offset:2048\n\t"
-        "ds_read_b128 %3, %8 offset:3072\n\t"
+        "ds_read_b128 %1, %8 offset:%10\n\t"
+        "ds_read_b128 %2, %8 offset:%11\n\t"
+        "ds_read_b128 %3, %8 offset:%12\n\t"
         "ds_read_b128 %4, %9\n\t"
-        "ds_read_b128 %5, %9 offset:1024\n\t"
-        "ds_read_b128 %6, %9 offset:2048\n\t"
-        "ds_read_b128 %7, %9 offset:3072\n\t"
+        "ds_read_b128 %5, %9 offset:%10\n\t"
+        "ds_read_b128 %6, %9 offset:%11\n\t"
+        "ds_read_b128 %7, %9 offset:%12\n\t"
         "s_waitcnt lgkmcnt(0)"
         : "=&v"(f[0]), "=&v"(f[1]), "=&v"(f[2]), "=&v"(f[3]), "=&v"(f[4]), "=&v"(f[5]),
           "=&v"(f[6]), "=&v"(f[7])
-        : "v"(wa), "v"(xa)
+        : "v"(wa), "v"(xa), "i"(F), "i"(2 * F), "i"(3 * F)
         : "memory");
 }
 
@@ -1028,20 +1035,25 @@ __device__ __forceinline__ void sk_wait(int n) {
 
 // y[r0 + r][n0 .. n0 + 63] = w_down[e_first + e][n0 ..] . act[r0 + r] for
 // the r < rows of expert e (offsets indexed by e_first + e, as in the other
-// launches); grid = e_count * (N / SK_BN), ns ring stages.
-template <int BM>
+// launches); grid = e_count * (N / SK_BN), ns ring stages of BK K.
+template <int BM, int BK>
 __global__ __launch_bounds__(64) void skinny_down_kernel(const int32_t *__restrict__ offsets,
                                                          int e_first, int e_count,
                                                          const bf16_t *__restrict__ act,
                                                          const bf16_t *__restrict__ w,
                                                          int64_t wstride, int N, int K,
                                                          float *__restrict__ y, int ns) {
-    constexpr int BK = SK_BK;
     constexpr int TN = SK_BN / 16, TM = BM / 16;
-    static_assert(TM <= 4, "at most 4 act fragments per stage");
-    constexpr int WI = SK_BN / 16, XI = BM / 16;  // LDS-DMA requests (16 rows x 64 bytes)
+    static_assert(TM <= 4, "at most 4 act fragments per K-step");
+    static_assert(BK == 32 || BK == 64, "16-byte chunks: 4 or 8 per LDS row");
+    constexpr int CPR = BK / 8;    // 16-byte chunks per LDS row
+    constexpr int RPI = 64 / CPR;  // rows one LDS-DMA request fills
+    constexpr int WI = SK_BN / RPI, XI = BM / RPI;
     constexpr int LPS = WI + XI;
+    static_assert(LPS == sk_lps(BM, BK), "requests per stage");
     constexpr int STAGE = (SK_BN + BM) * BK;  // bf16 elements
+    constexpr int F = 16 * BK * 2;            // bytes of 16 LDS rows
+    constexpr int KH = BK / 32;               // MFMA K-steps per stage
     // ring of ns stages (2 <= ns <= sk_ahead_max(LPS) + 1), sk_lds_bytes
     extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
 
@@ -1055,17 +1067,18 @@ __global__ __launch_bounds__(64) void skinny_down_kernel(const int32_t *__restri
     const int lane = threadIdx.x;
     const int64_t n0 = (int64_t)nt * SK_BN;
 
-    // LDS-DMA sources: lane i fetches row (i / 4) of a 16-row request, the
-    // 16-byte chunk (i % 4) ^ swz(row) of the stage's 32 K, into place i % 4
-    const int drow = lane >> 2;
-    const int dchunk = ((lane & 3) ^ swz<BK>(drow)) * 8;
+    // LDS-DMA sources: lane i fetches row (i / CPR) of an RPI-row request,
+    // the 16-byte chunk (i % CPR) ^ swz(row) of the stage's BK K, into
+    // place i % CPR
+    const int drow = lane / CPR;
+    const int dchunk = ((lane % CPR) ^ swz<BK>(drow)) * 8;
     const bf16_t *src[LPS];
     const bf16_t *we = w + (int64_t)(e_first + e) * wstride;
 #pragma unroll
-    for (int i = 0; i < WI; ++i) src[i] = we + (n0 + i * 16 + drow) * K + dchunk;
+    for (int i = 0; i < WI; ++i) src[i] = we + (n0 + i * RPI + drow) * K + dchunk;
 #pragma unroll
     for (int i = 0; i < XI; ++i) {
-        const int j = min(i * 16 + drow, rows - 1);  // rows past the expert's: repeats
+        const int j = min(i * RPI + drow, rows - 1);  // rows past the expert's: repeats
         src[WI + i] = act + (int64_t)(r0 + j) * K + dchunk;
     }
     const int nk = K / BK;
@@ -1074,16 +1087,21 @@ __global__ __launch_bounds__(64) void skinny_down_kernel(const int32_t *__restri
 #pragma unroll
         for (int i = 0; i < LPS; ++i)
             __builtin_amdgcn_global_load_lds((gbl_void_t *)(src[i] + kt * BK),
-                                             (lds_void_t *)(sb + i * 16 * BK), 16, 0, 0);
+                                             (lds_void_t *)(sb + i * RPI * BK), 16, 0, 0);
     };
 
-    // fragment addresses in ring slot 0: weight row t * 16 + lrow and act
-    // row m * 16 + lrow, the chunk holding K 8 (lane / 16) .. + 7
+    // fragment addresses in ring slot 0, K-step h of the stage: weight row
+    // t * 16 + lrow and act row m * 16 + lrow, the chunk holding K
+    // 32 h + 8 (lane / 16) .. + 7
     const int lrow = lane & 15;
-    const int chunk = ((lane >> 4) ^ swz<BK>(lrow)) * 8;
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void_t *)smem;
-    const uint32_t wa0 = lds0 + (uint32_t)((lrow * BK + chunk) * 2);
-    const uint32_t xa0 = wa0 + (uint32_t)(SK_BN * BK * 2);
+    uint32_t wa0[KH], xa0[KH];
+#pragma unroll
+    for (int h = 0; h < KH; ++h) {
+        const int chunk = ((h * 4 + (lane >> 4)) ^ swz<BK>(lrow)) * 8;
+        wa0[h] = lds0 + (uint32_t)((lrow * BK + chunk) * 2);
+        xa0[h] = wa0[h] + (uint32_t)(SK_BN * BK * 2);
+    }
 
     floatx4 acc[TN][TM];
 #pragma unroll
@@ -1102,14 +1120,17 @@ __global__ __launch_bounds__(64) void skinny_down_kernel(const int32_t *__restri
         sk_wait<LPS>(min(ahead, nk - 1 - kt));  // stage kt landed
         const uint32_t so = (uint32_t)(rslot * STAGE * 2);
         rslot = rslot + 1 == ns ? 0 : rslot + 1;
-        bf16x8 f[8];
-        sk_read_frags(f, wa0 + so, xa0 + so);
 #pragma unroll
-        for (int m = 0; m < TM; ++m)
+        for (int h = 0; h < KH; ++h) {
+            bf16x8 f[8];
+            sk_read_frags<F>(f, wa0[h] + so, xa0[h] + so);
 #pragma unroll
-            for (int t = 0; t < TN; ++t)
-                acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f[t], f[4 + m], acc[t][m],
-                                                                    0, 0, 0);
+            for (int m = 0; m < TM; ++m)
+#pragma unroll
+                for (int t = 0; t < TN; ++t)
+                    acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f[t], f[4 + m],
+                                                                        acc[t][m], 0, 0, 0);
+        }
     }
 
     // epilogue: the lane holds output columns t * 16 + 4 (lane / 16) .. + 3
@@ -1128,24 +1149,24 @@ __global__ __launch_bounds__(64) void skinny_down_kernel(const int32_t *__restri
 // Ring depth of a launch of `tiles` non-empty tiles: the deepest ring (at
 // most sk_ahead_max + 1 stages, SK_LDS_MAX bytes) with which the tiles of a
 // compute unit all fit its LDS at once, and at least 4 stages.
-int sk_ring(int bm, int64_t tiles) {
-    const int lps = SK_BN / 16 + bm / 16;
+int sk_ring(int bm, int bk, int64_t tiles) {
     const int cus = device_cu_count();
     const int64_t per_cu = std::max<int64_t>(1, (tiles + cus - 1) / cus);
     const size_t cap = std::min<size_t>(SK_LDS_MAX, (size_t)(160 * 1024) / per_cu);
-    int ns = sk_ahead_max(lps) + 1;
-    while (ns > 4 && sk_lds_bytes(bm, ns) > cap) --ns;
+    int ns = sk_ahead_max(sk_lps(bm, bk)) + 1;
+    while (ns > 4 && sk_lds_bytes(bm, bk, ns) > cap) --ns;
     return ns;
 }
 
-template <int BM>
-hipError_t skinny_down_launch(unsigned blocks, int ns, const int32_t *offsets, int e_first,
-                              int e_count, const bf16_t *act, const bf16_t *w, int64_t wstride,
-                              int N, int K, float *y, hipStream_t s) {
-    constexpr int LPS = SK_BN / 16 + BM / 16;
-    if (ns < 2 || ns - 1 > sk_ahead_max(LPS) || sk_lds_bytes(BM, ns) > SK_LDS_MAX)
+template <int BM, int BK>
+hipError_t skinny_down_launch(unsigned blocks, int64_t tiles, const int32_t *offsets,
+                              int e_first, int e_count, const bf16_t *act, const bf16_t *w,
+                              int64_t wstride, int N, int K, float *y, hipStream_t s) {
+    if (K % BK) return hipErrorInvalidValue;
+    const int ns = sk_ring(BM, BK, tiles);
+    if (ns < 2 || ns - 1 > sk_ahead_max(sk_lps(BM, BK)) || sk_lds_bytes(BM, BK, ns) > SK_LDS_MAX)
         return hipErrorInvalidValue;
-    skinny_down_kernel<BM><<<blocks, 64, sk_lds_bytes(BM, ns), s>>>(
+    skinny_down_kernel<BM, BK><<<blocks, 64, sk_lds_bytes(BM, BK, ns), s>>>(
         offsets, e_first, e_count, act, w, wstride, N, K, y, ns);
     return hipGetLastError();
 }
@@ -1402,18 +1423,18 @@ hipError_t launch_skinny_down(const moe_dims &d, int e_first, int e_count,
     if (N % SK_BN || K % SK_BK) return hipErrorInvalidValue;
     const unsigned blocks = (unsigned)(e_count * (N / SK_BN));
     const int64_t active = std::min<int64_t>(e_count, std::max<int64_t>(1, active_experts));
-    const int ns = sk_ring(bm, active * (N / SK_BN));
+    const int64_t tiles = active * (N / SK_BN);
     const int64_t wstride = (int64_t)N * K;
     switch (bm) {
         case 16:
-            return skinny_down_launch<16>(blocks, ns, offsets, e_first, e_count, act, w_down,
-                                          wstride, N, K, y_perm, s);
+            return skinny_down_launch<16, SK_BK>(blocks, tiles, offsets, e_first, e_count, act,
+                                                 w_down, wstride, N, K, y_perm, s);
         case 32:
-            return skinny_down_launch<32>(blocks, ns, offsets, e_first, e_count, act, w_down,
-                                          wstride, N, K, y_perm, s);
+            return skinny_down_launch<32, SK_BK>(blocks, tiles, offsets, e_first, e_count, act,
+                                                 w_down, wstride, N, K, y_perm, s);
         case 64:
-            return skinny_down_launch<64>(blocks, ns, offsets, e_first, e_count, act, w_down,
-                                          wstride, N, K, y_perm, s);
+            return skinny_down_launch<64, SK_BK>(blocks, tiles, offsets, e_first, e_count, act,
+                                                 w_down, wstride, N, K, y_perm, s);
         default:
             return hipErrorInvalidValue;
     }

@@ -202,12 +202,14 @@ def test_workspace_guards_untouched(name, kw):
 # Decode-sized shapes whose grouped down GEMM takes the skinny tile (at most
 # 64 rows per expert, at least two 64-column tiles per compute unit of a
 # 256-CU device): tile rows 16, 32 and 64, K shorter than the LDS ring,
-# a local window whose later pipeline stages start at expert e_first > 0.
+# more tiles per compute unit than fit its LDS at once, a local window
+# whose later pipeline stages start at expert e_first > 0.
 @pytest.mark.parametrize("T,E,EL,e0,k,H,I,shared", [
     (5, 64, 64, 0, 8, 1024, 256, 0),      # 16-row tiles
     (64, 8, 8, 0, 2, 4096, 256, 0),       # 32-row tiles
     (64, 4, 4, 0, 2, 8192, 128, 0),       # 64-row tiles; 4 K stages
     (64, 2, 2, 0, 2, 16384, 64, 0),       # every expert exactly 64 rows
+    (64, 4, 4, 0, 2, 16384, 128, 0),      # 64-row tiles, 4 per CU (2 resident at once)
     (48, 32, 16, 8, 8, 4096, 128, 0),     # a local window; PN = 2 stays skinny
     (40, 160, 160, 0, 6, 512, 256, 512),  # many experts, most empty; shared FFN
 ])

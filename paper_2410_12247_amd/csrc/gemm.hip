@@ -330,23 +330,31 @@ __device__ __forceinline__ void run_tile(const TileArgs &a, bf16_t *smem) {
 // eight waves in two groups of four, one wave of each group on every SIMD.
 // Each wave owns a 128 x BM/4 accumulator block.  The groups alternate
 // between a compute phase (MFMAs on fragments already in registers) and a
-// memory phase (its share of the LDS-DMA for stage k+3 and the fragment
+// memory phase (its share of the LDS-DMA for stage k+NS-1 and the fragment
 // reads of its next stage), separated by workgroup barriers, so every SIMD
 // always has one wave issuing MFMAs while the other feeds LDS.  Stage s
-// lives in LDS buffer s % 4.
-//   group A (waves 0-3, token rows 0..BM/2-1):  compute(k) | mem: frags(k+1), DMA(k+3)
-//   group B (waves 4-7, token rows BM/2..BM-1): mem: frags(k), DMA(k+3) | compute(k)
+// lives in LDS buffer s % NS (NS = 4 stages of 32 K, or 3 of 64 K).
+//   group A (waves 0-3, token rows 0..BM/2-1):  compute(k) | mem: frags(k+1), DMA(k+NS-1)
+//   group B (waves 4-7, token rows BM/2..BM-1): mem: frags(k), DMA(k+NS-1) | compute(k)
 // LDS traffic per MFMA falls as the wave tile grows: BM = 320 (wave tile
 // 128 x 80, 40 MFMAs per 13 fragment reads, 160 accumulator registers, four
 // 36 KiB stages) is the largest that fits 256 registers and 160 KiB of LDS.
 // ---------------------------------------------------------------------------
 constexpr int PP_THREADS = 512;
+// K per LDS stage of the ping-pong tile of bm token rows: 64 for the
+// 128-row tile (decode-sized launches, bound by the weight stream, read 128
+// contiguous bytes of each weight row per stage instead of 64: about 10%
+// faster on 64-token decode), 32 for the taller, MFMA-bound tiles
+__host__ __device__ constexpr int pp_stage_k(int bm) { return bm == 128 ? 64 : 32; }
 // buffer resource word 3 for raw (untyped, unswizzled) access on gfx9 parts
 constexpr int kBufferFlags = 0x00020000;
 
 template <int MODE, int BM_>
 struct PPCfg {
-    static constexpr int BN = 256, BM = BM_, BK = 32, NS = 4;
+    static constexpr int BN = 256, BM = BM_;
+    static constexpr int BK = pp_stage_k(BM_);
+    static constexpr int NS = BK == 64 ? 3 : 4;  // ring within 144 KB of LDS
+    static constexpr int KH = BK / 32;  // MFMA K-steps per stage
     static constexpr int WTN = 128, WTM = BM / 4;  // wave tile (weights x tokens)
     static constexpr int TN = WTN / 16, TM = WTM / 16;
     static_assert(WTM % 16 == 0, "token rows per wave: whole 16-row fragments");
@@ -363,6 +371,8 @@ struct PPCfg {
     static constexpr int LPS_B = W_INSTR + X_INSTR_B;
     static constexpr int STAGE_W = BN * BK, STAGE_X = BM * BK, STAGE = STAGE_W + STAGE_X;
     static constexpr int LDS_ELEMS = NS * STAGE;
+    static_assert(LDS_ELEMS * 2 <= 144 * 1024, "ring within 144 KB of LDS");
+    static_assert(NS >= 3 && (NS - 2) * (LPS_A > LPS_B ? LPS_A : LPS_B) <= 63, "vmcnt range");
     static constexpr int BNOUT = MODE == 0 ? BN / 2 : BN;
     static constexpr int PART_ELEMS = BN * BM;  // fp32 accumulators of one tile
     static constexpr int PART_BYTES = PART_ELEMS * 4;
@@ -505,29 +515,38 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
             arow[t] = wn * C::WTN + t * 16;
     }
     const int lrow = lane & 15;
-    const int chunk = ((lane >> 4) ^ swz<BK>(lrow)) * 8;
-    bf16x8 fa[C::TN], fb[C::TM];
+    // the chunk holding K 32 h + 8 (lane / 16) .. + 7 of a row, K-step h
+    int chunk[C::KH];
+#pragma unroll
+    for (int h = 0; h < C::KH; ++h) chunk[h] = ((h * 4 + (lane >> 4)) ^ swz<BK>(lrow)) * 8;
+    bf16x8 fa[C::KH][C::TN], fb[C::KH][C::TM];
     auto load_frags = [&](int kstage) {  // stale but in-bounds past the end
         const bf16_t *sw = smem + (kstage % NS) * C::STAGE;
         const bf16_t *sx = sw + C::STAGE_W;
 #pragma unroll
-        for (int t = 0; t < C::TN; ++t)
-            fa[t] = *reinterpret_cast<const bf16x8 *>(sw + (arow[t] + lrow) * BK + chunk);
-#pragma unroll
-        for (int m = 0; m < C::TM; ++m)
-            fb[m] = *reinterpret_cast<const bf16x8 *>(sx + (wm * C::WTM + m * 16 + lrow) * BK +
-                                                      chunk);
-    };
-    auto mfmas = [&]() {
-#pragma unroll
-        for (int m = 0; m < C::TM; ++m)
+        for (int h = 0; h < C::KH; ++h) {
 #pragma unroll
             for (int t = 0; t < C::TN; ++t)
-                acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[t], fb[m], acc[t][m], 0,
-                                                                    0, 0);
+                fa[h][t] =
+                    *reinterpret_cast<const bf16x8 *>(sw + (arow[t] + lrow) * BK + chunk[h]);
+#pragma unroll
+            for (int m = 0; m < C::TM; ++m)
+                fb[h][m] = *reinterpret_cast<const bf16x8 *>(
+                    sx + (wm * C::WTM + m * 16 + lrow) * BK + chunk[h]);
+        }
+    };
+    auto mfmas = [&]() {  // K-steps in ascending order
+#pragma unroll
+        for (int h = 0; h < C::KH; ++h)
+#pragma unroll
+            for (int m = 0; m < C::TM; ++m)
+#pragma unroll
+                for (int t = 0; t < C::TN; ++t)
+                    acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[h][t], fb[h][m],
+                                                                        acc[t][m], 0, 0, 0);
     };
 
-    // prologue: stages 0..2 requested by every wave, all landed
+    // prologue: stages 0 .. NS-2 requested by every wave, all landed
     using nxa = std::integral_constant<int, C::X_INSTR_A>;
     using nxb = std::integral_constant<int, C::X_INSTR_B>;
 #pragma unroll
@@ -547,10 +566,11 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
             __builtin_amdgcn_s_setprio(1);
             if constexpr (decltype(with_mfma)::value) mfmas();
             __builtin_amdgcn_s_setprio(0);
-            // stage k+1 (requested two iterations ago) landed before the barrier
-            wait_vmcnt<C::LPS_A>();
+            // stage k+1 landed before the barrier; this wave's requests for
+            // stages k+2 .. k+NS-2 may stay in flight
+            wait_vmcnt<(NS - 3) * C::LPS_A>();
             __builtin_amdgcn_s_barrier();
-            // memory phase: fragments of stage k+1, this wave's share of stage k+3
+            // memory phase: fragments of stage k+1, this wave's share of stage k+NS-1
             load_frags(k + 1);
             issue(k + NS - 1, nxa{});
             __builtin_amdgcn_s_barrier();
@@ -558,12 +578,12 @@ __device__ __forceinline__ void run_tile_pp(const TileArgs &a, bf16_t *smem) {
     };
     auto loop_b = [&](auto with_mfma) {
         for (int k = 0; k < nk; ++k) {
-            // memory phase: fragments of stage k, this wave's share of stage k+3
+            // memory phase: fragments of stage k, this wave's share of stage k+NS-1
             load_frags(k);
             issue(k + NS - 1, nxb{});
-            // stage k+1 (requested in iteration k-2) landed; the requests of
-            // iterations k-1 and k may stay in flight
-            wait_vmcnt<2 * C::LPS_B>();
+            // stage k+1 landed; this wave's requests for stages k+2 ..
+            // k+NS-1 (the last just issued) may stay in flight
+            wait_vmcnt<(NS - 2) * C::LPS_B>();
             __builtin_amdgcn_s_barrier();
             // compute phase: stage k
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -1254,35 +1274,35 @@ hipError_t dense_launch_bm(int bm, int64_t rows, const bf16_t *x, const bf16_t *
 // ---- launch cost model (host) ---------------------------------------------
 // Device time of one launch of the persistent scheduler, from per-tile costs
 // of each tile height measured on MI355X (microseconds):
-//   tile time = nk * step(MODE, BM) + epi(MODE, BM)
-// where nk is the number of 32-deep K stages.  Tiles run in rounds of G
+//   tile time = K / 32 * step(MODE, BM) + epi(MODE, BM)
+// (step: the cost of 32 K, whatever the tile's stage depth).  Tiles run in rounds of G
 // workgroups; a partial round of rem tiles takes the fraction
 // kPartialRound[MODE] + (1 - kPartialRound) * busy of a full round's K loop
 // (busy = the fraction of workgroups with work: fewer active compute units
 // run each tile faster), then the epilogue.  With the K split, a partial
 // last round of rem <= G/2 tiles is cut into S pieces as the scheduler does
-// (S = min(8, G/rem, nk/32, slots/rem)): its K loop is S times shorter, and
+// (S = min(8, G/rem, stages/32, slots/rem)): its K loop is S times shorter, and
 // the fixup costs a fixed time plus a time per partial-sum block (its bytes
 // grow with BM).  Each launch pays a fixed start-up and drain time.
 struct TileCost {
     int bm;
-    double step_us[2];  // one 32-deep K stage of a 256 x BM tile: gate/up, down
+    double step_us[2];  // 32 K of a 256 x BM tile: gate/up, down
     double epi_us[2];   // a tile's epilogue: gate/up (bf16 SiLU*mul), down (fp32)
 };
-// Fitted by least squares (4.5% rms, 14% worst) to one expert's dense
-// launches at 512 .. 32768 rows on the DeepSeekV2 (H 5120, I 1536) and
-// Mixtral (H 4096, I 3584) expert shapes, every tile height, with and
-// without the K split (bench.py --tile-study).
+// Fitted by least squares (4.0% rms gate/up, 4.5% down, 14% worst) to one
+// expert's dense launches at 512 .. 32768 rows on the DeepSeekV2 (H 5120,
+// I 1536) and Mixtral (H 4096, I 3584) expert shapes, every tile height,
+// with and without the K split (bench.py --tile-study).
 constexpr TileCost kTileCosts[] = {
-    {320, {0.912, 0.995}, {10.4, 10.9}},
-    {256, {0.757, 0.832}, {11.6, 11.9}},
-    {192, {0.630, 0.699}, {6.0, 8.2}},
-    {128, {0.557, 0.561}, {0.0, 7.4}},
+    {320, {0.896, 1.004}, {13.0, 12.3}},
+    {256, {0.750, 0.839}, {14.6, 12.8}},
+    {192, {0.607, 0.715}, {10.7, 9.3}},
+    {128, {0.441, 0.471}, {6.2, 7.7}},
 };
-constexpr double kLaunchUs[2] = {13.5, 7.5};     // start-up + drain: gate/up, down
-constexpr double kPartialRound[2] = {0.71, 0.72};
-constexpr double kFixupUs[2] = {4.7, 2.2};       // fixup launch with work
-constexpr double kFixupBlockUs[2] = {0.0795, 0.0741};  // per 256 x 320 partial block
+constexpr double kLaunchUs[2] = {12.9, 6.4};     // start-up + drain: gate/up, down
+constexpr double kPartialRound[2] = {0.69, 0.71};
+constexpr double kFixupUs[2] = {0.0, 2.3};       // fixup launch with work
+constexpr double kFixupBlockUs[2] = {0.0994, 0.0864};  // per 256 x 320 partial block
 
 const TileCost &tile_cost(int bm) {
     for (const TileCost &c : kTileCosts)
@@ -1296,8 +1316,8 @@ double gemm_launch_us(int mode, int bm, int64_t tiles, int K, int grid, bool spl
     if (tiles <= 0) return 0.0;
     const TileCost &c = tile_cost(bm);
     const int md = mode ? 1 : 0;
-    const int nk = K / 32;
-    const double loop_us = nk * c.step_us[md];
+    const double loop_us = K / 32 * c.step_us[md];
+    const int nk = K / pp_stage_k(bm);  // the tile's K stages, as the kernel cuts them
     const int64_t full_rounds = tiles / grid;
     const int64_t rem = tiles % grid;
     double us = kLaunchUs[md] + full_rounds * (loop_us + c.epi_us[md]);

@@ -58,6 +58,8 @@ def parse_args(argv=None):
                    help="pipeline stages: expert groups (default) or token ranges")
     p.add_argument("--cu-budget", type=int, default=0)
     p.add_argument("--dense-min-rows", type=int, default=0)
+    p.add_argument("--group-tile-rows", type=int, default=0,
+                   help="force the GroupGemm tile height (128, 192, 256, 320; 0 = model)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU time of the oracle baseline sample")
@@ -169,7 +171,7 @@ def run_workload(args, shape, inp, steps, warmup, timing=True, serial=False, dev
     chunk = {"experts": moe.CHUNK_EXPERTS, "tokens": moe.CHUNK_TOKENS}[args.chunk_mode]
     o = moe.opts(gemm_mode=mode, pipeline_n=args.pn, gemm_cu_budget=args.cu_budget,
                  dense_min_rows=args.dense_min_rows, timing=timing, chunk_mode=chunk,
-                 serial=serial, side_cus=args.side_cus)
+                 serial=serial, side_cus=args.side_cus, group_tile_rows=args.group_tile_rows)
     g = dev_inputs if dev_inputs is not None else DeviceInputs(inp)
     buf = g.buffers(o)
 
@@ -336,6 +338,7 @@ def main(argv=None):
                    "gemm_mode": args.mode, "pipeline_n": args.pn,
                    "chunk_mode": args.chunk_mode,
                    "gemm_cu_budget": args.cu_budget, "side_cus": args.side_cus,
+                   "group_tile_rows": args.group_tile_rows,
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm" if hbm_bound else "mfma", "achieved": round(achieved, 1),
                      "peak": peak, "unit": "GB/s" if hbm_bound else "TFLOP/s",

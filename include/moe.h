@@ -135,6 +135,11 @@ typedef struct {
                                streams run on this many CUs (spread over the
                                XCDs) and the GEMM stream, with its persistent
                                grid, on the others.  At most 248. */
+    int32_t group_tile_rows;/* token rows of a GroupGemm tile: 0 = chosen per
+                               stage by the launch-cost model (never taller
+                               than the smallest height that holds the
+                               stage's largest expert), or 128, 192, 256,
+                               320 to force one */
 } moe_opts;
 
 /* Per-phase device time, in milliseconds summed over stages and over the
@@ -354,13 +359,15 @@ moe_status moe_pipeline_plan(const moe_dims *dims, const moe_opts *opts, const i
  * with one expert per stage the grouped GEMM becomes a dense one), from the
  * host row counts of its n_experts experts, rows[0..n_experts).  The model
  * prices each launch from measured per-tile costs of every tile height:
- * GroupGemm is one launch over the stage with 320-row tiles; DenseGemm is
- * one launch per expert with its own tile height.  Writes *dense (1 when
+ * GroupGemm is one launch over the stage with one tile height (the model's
+ * cheapest up to the smallest height that holds the largest expert, taken
+ * when at least 5% below that height's price; or opts->group_tile_rows);
+ * DenseGemm is one launch per expert with its own tile height.  Writes *dense (1 when
  * the stage would run DenseGemm under opts->gemm_mode, AUTO included) and,
  * when not NULL, tile_rows[e] (the tile height of expert e's launch, 0 for
  * an empty expert), *group_us and *dense_us (predicted GEMM microseconds
  * of the two kinds).  Uses dims->hidden / inter, opts->gemm_cu_budget,
- * dense_min_rows, dense_tile_rows and MOE_FLAG_EXACT_ORDER.  Host-only;
+ * dense_min_rows, dense_tile_rows, group_tile_rows and MOE_FLAG_EXACT_ORDER.  Host-only;
  * never touches the GPU (the grid is the current device's CU count, 256
  * when no device is visible). */
 moe_status moe_gemm_plan(const moe_dims *dims, const moe_opts *opts, int32_t n_experts,

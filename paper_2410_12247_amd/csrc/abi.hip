@@ -230,9 +230,11 @@ moe_status moe_ffn_group(const moe_dims *dims, int32_t e_first, int32_t e_count,
     int grid = cu_budget > 0 ? cu_budget : device_cu_count();
     grid = std::max(8, (grid / 8) * 8);
     hipStream_t s = (hipStream_t)stream;
-    // no workspace here: every tile covers the whole K range in one pass
+    // no workspace here: every tile covers the whole K range in one pass;
     // no expert has more rows than there are tokens
-    const int bm = group_tile_rows(dims->tokens);
+    const int bm = group_launch_rows(dims->tokens, nullptr, e_count, dims->tokens,
+                                     (double)dims->top_k / dims->experts, dims->hidden,
+                                     dims->inter, grid, false);
     MOE_HIP(launch_group_gateup(*dims, e_first, e_count, offsets, x_perm, nullptr, w_gate, w_up,
                                 act, grid, nullptr, nullptr, bm, s));
     // decode-sized experts with enough tiles: the skinny down tile

@@ -178,6 +178,19 @@ int dense_tile_rows(int64_t rows, int H, int I, int grid, bool split);
 // max_rows rows (the launch's tokens bound it: a token routes to an expert
 // at most once): 320, or the smallest height that holds max_rows below it.
 int group_tile_rows(int64_t max_rows);
+// The tile height of a grouped launch over n_experts experts, none with more
+// than max_rows rows: the launch-cost model prices each height up to
+// group_tile_rows(max_rows) (gate/up over K = H, down over K = I) and the
+// cheapest is taken when it is at least kGroupRowsMinGain below that
+// height's price.  Shorter tiles pad less: for experts of a few rows each
+// (decode batches, many experts) every tile is mostly padding, and the
+// 128-row tile streams the weights faster.  rows: the experts' host row
+// counts, or NULL when only the bound is known: then each expert's rows are
+// taken as Binomial(tokens, p) (p = top_k / experts, uniform routing) and
+// its tile counts as their expectation.
+constexpr double kGroupRowsMinGain = 0.05;
+int group_launch_rows(int64_t max_rows, const int32_t *rows, int n_experts, int64_t tokens,
+                      double p, int H, int I, int grid, bool split);
 // Skinny down GEMM for decode-sized grouped launches: one wave per tile of
 // 64 output columns by an expert's rows (at most 64) over the whole K
 // range, no K split (the same bits as every other tile height in exact

@@ -242,6 +242,9 @@ moe_status check_opts(const moe_dims *d, const moe_opts *o) {
                     o->dense_tile_rows);
     if (o->side_cus < 0 || o->side_cus > kMaxExperts - 8)
         return fail(MOE_ERR_INVALID, "side_cus %d outside [0, 248]", o->side_cus);
+    if (o->group_tile_rows != 0 && !valid_tile_rows(o->group_tile_rows))
+        return fail(MOE_ERR_INVALID, "group_tile_rows %d is not 0, 128, 192, 256 or 320",
+                    o->group_tile_rows);
     return MOE_OK;
 }
 
@@ -277,7 +280,9 @@ bool auto_picks_dense(const moe_dims &d, const moe_opts &o, const int32_t *rows,
                       bool split, double *group_us, double *dense_us) {
     int32_t max_rows = 0;
     for (int e = 0; e < n; ++e) max_rows = std::max(max_rows, rows[e]);
-    const int bm_g = group_tile_rows(max_rows);
+    const int bm_g = o.group_tile_rows > 0 ? o.group_tile_rows
+                                           : group_launch_rows(max_rows, rows, n, 0, 0.0, d.hidden,
+                                                               d.inter, grid, split);
     int64_t tiles_gu = 0, tiles_dn = 0;
     double dus = 0.0;
     int32_t min_rows = INT32_MAX;
@@ -561,11 +566,13 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         MOE_TRY(tm.begin(sm, PH_SHARED));
         shared_offsets_kernel<<<1, 64, 0, sm>>>(soff, (int32_t)T);
         MOE_HIP(hipGetLastError());
+        // one expert of T rows, known on the host: the height a dense
+        // launch of those rows takes
+        const int bm_s = dense_tile_rows(T, H, d.shared_inter, grid, split);
         MOE_HIP(launch_group_gateup(ds, 0, 1, soff, x, nullptr, shared_gate, shared_up,
-                                    shared_act, grid, split_part, split_meta, group_tile_rows(T),
-                                    sm));
+                                    shared_act, grid, split_part, split_meta, bm_s, sm));
         MOE_HIP(launch_group_down(ds, 0, 1, soff, shared_act, shared_down, y, grid, split_part,
-                                  split_meta, group_tile_rows(T), sm));
+                                  split_meta, bm_s, sm));
         MOE_TRY(tm.end(sm));
     }
 
@@ -699,7 +706,12 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
             // read on the device
             if (timing) ++g_timing.group_stages;
             if (stage_rows > 0) {
-                const int bm = group_tile_rows(stage_max_rows);
+                const int bm =
+                    o->group_tile_rows > 0
+                        ? o->group_tile_rows
+                        : group_launch_rows(stage_max_rows, need_counts ? &hc[b0] : nullptr,
+                                            per_stage, t_hi - t_lo, (double)d.top_k / d.experts,
+                                            H, I, grid, split);
                 MOE_TRY(tm.begin(sm, PH_GATEUP));
                 MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, xrows, rmap, w_gate, w_up,
                                             act, grid, split_part, split_meta, bm, sm));
@@ -801,7 +813,10 @@ moe_status moe_gemm_plan(const moe_dims *dims, const moe_opts *opts, int32_t n_e
     for (int e = 0; e < n_experts; ++e) max_rows = std::max(max_rows, rows[e]);
     if (tile_rows)
         for (int e = 0; e < n_experts; ++e)
-            tile_rows[e] = !d_ ? group_tile_rows(max_rows)
+            tile_rows[e] = !d_ ? (o->group_tile_rows > 0
+                                      ? o->group_tile_rows
+                                      : group_launch_rows(max_rows, rows, n_experts, 0, 0.0,
+                                                          dims->hidden, dims->inter, grid, split))
                            : rows[e] == 0 ? 0
                            : o->dense_tile_rows > 0
                                ? o->dense_tile_rows

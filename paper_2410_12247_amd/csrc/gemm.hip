@@ -32,6 +32,7 @@
 // round-robin over the 8 XCDs), so the tiles running on one XCD are
 // neighbours in (m, n) and share activation and weight rows in its L2.
 #include <algorithm>
+#include <cmath>
 #include <type_traits>
 
 #include "common.h"
@@ -969,11 +970,12 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(const float *__restric
 }
 
 // Tile policy of each scheduler: the ping-pong tile, 256 weight rows by BM
-// token rows.  The grouped launch knows only a bound on its experts' rows
-// (the tokens, or the largest host count) and takes the tallest tile
-// (BM = 320, fewest LDS bytes per MFMA) unless a smaller height holds that
-// bound (group_tile_rows); a dense launch knows its expert's rows and takes
-// the height whose tile count fills the grid best (dense_tile_rows).
+// token rows.  The grouped launch knows its experts' host row counts or
+// only a bound on them (the tokens); the launch-cost model picks its height
+// (group_launch_rows) up to the smallest that holds that bound, with 320
+// rows (fewest LDS bytes per MFMA) above 256; a dense launch knows its
+// expert's rows and takes the height whose tile count fills the grid best
+// (dense_tile_rows).
 #ifndef MOE_GEMM_PINGPONG
 #define MOE_GEMM_PINGPONG 1
 #endif
@@ -1380,6 +1382,86 @@ int group_tile_rows(int64_t max_rows) {
 #endif
     (void)max_rows;
     return kTokenTile;
+}
+
+namespace {
+
+constexpr int kTileHeights[4] = {128, 192, 256, 320};
+
+// Expected m-tiles of one expert for each tile height, E[ceil(min(r, cap)
+// / bm)], where its row count r ~ Binomial(tokens, p): every token picks
+// the expert with probability p (top_k distinct of E experts, uniform).
+// The probabilities are walked out from the mode by the ratio of
+// neighbouring terms until they fall below 1e-12 of the mode's.
+void expected_mtiles(int64_t tokens, double p, int64_t cap, double out[4]) {
+    for (int i = 0; i < 4; ++i) out[i] = 0.0;
+    if (tokens <= 0 || cap <= 0 || p <= 0.0) return;
+    auto add = [&](int64_t r, double pr) {
+        const int64_t rr = std::min(r, cap);
+        for (int i = 0; i < 4; ++i) out[i] += pr * (double)((rr + kTileHeights[i] - 1) / kTileHeights[i]);
+    };
+    if (p >= 1.0) {
+        add(tokens, 1.0);
+        return;
+    }
+    const double q = 1.0 - p, n = (double)tokens;
+    const int64_t mode = std::min<int64_t>(tokens, (int64_t)((n + 1.0) * p));
+    const double m = (double)mode;
+    const double pm = std::exp(std::lgamma(n + 1.0) - std::lgamma(m + 1.0) -
+                               std::lgamma(n - m + 1.0) + m * std::log(p) + (n - m) * std::log(q));
+    double total = pm, pr = pm;
+    add(mode, pm);
+    for (int64_t r = mode; r < tokens; ++r) {
+        pr *= (double)(tokens - r) / (double)(r + 1) * (p / q);
+        if (pr < 1e-12 * pm) break;
+        add(r + 1, pr);
+        total += pr;
+    }
+    pr = pm;
+    for (int64_t r = mode; r > 0; --r) {
+        pr *= (double)r / (double)(tokens - r + 1) * (q / p);
+        if (pr < 1e-12 * pm) break;
+        add(r - 1, pr);
+        total += pr;
+    }
+    for (int i = 0; i < 4; ++i) out[i] /= total;
+}
+
+}  // namespace
+
+int group_launch_rows(int64_t max_rows, const int32_t *rows, int n_experts, int64_t tokens,
+                      double p, int H, int I, int grid, bool split) {
+    const int cap = group_tile_rows(max_rows);
+#if MOE_GEMM_PINGPONG
+    if (n_experts <= 0 || cap == kTileHeights[0]) return cap;
+    double mt[4];
+    if (rows == nullptr) expected_mtiles(tokens, p, max_rows, mt);
+    double us[4] = {0.0, 0.0, 0.0, 0.0};
+    int best = -1, icap = 0;
+    for (int i = 0; i < 4 && kTileHeights[i] <= cap; ++i) {
+        const int bm = kTileHeights[i];
+        int64_t tiles_gu = 0, tiles_dn = 0;
+        if (rows != nullptr) {
+            for (int e = 0; e < n_experts; ++e) {
+                tiles_gu += gemm_tiles(0, bm, rows[e], I);
+                tiles_dn += gemm_tiles(1, bm, rows[e], H);
+            }
+        } else {
+            const double m = n_experts * mt[i];
+            tiles_gu = std::llround(m * (double)gemm_tiles(0, bm, bm, I));
+            tiles_dn = std::llround(m * (double)gemm_tiles(1, bm, bm, H));
+        }
+        us[i] = gemm_launch_us(0, bm, tiles_gu, H, grid, split) +
+                gemm_launch_us(1, bm, tiles_dn, I, grid, split);
+        if (best < 0 || us[i] < us[best]) best = i;
+        icap = i;
+    }
+    // another height only for a predicted gain above the model's error
+    return us[best] < (1.0 - kGroupRowsMinGain) * us[icap] ? kTileHeights[best] : cap;
+#else
+    (void)rows, (void)n_experts, (void)tokens, (void)p, (void)H, (void)I, (void)grid, (void)split;
+    return cap;
+#endif
 }
 
 bool valid_tile_rows(int bm) {

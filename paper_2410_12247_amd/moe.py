@@ -46,7 +46,8 @@ class Opts(ctypes.Structure):
     _fields_ = [("gemm_mode", ctypes.c_int32), ("dense_min_rows", ctypes.c_int32),
                 ("pipeline_n", ctypes.c_int32), ("gemm_cu_budget", ctypes.c_int32),
                 ("flags", ctypes.c_int32), ("chunk_mode", ctypes.c_int32),
-                ("dense_tile_rows", ctypes.c_int32), ("side_cus", ctypes.c_int32)]
+                ("dense_tile_rows", ctypes.c_int32), ("side_cus", ctypes.c_int32),
+                ("group_tile_rows", ctypes.c_int32)]
 
 
 class Timing(ctypes.Structure):
@@ -127,7 +128,7 @@ def dims(tokens, hidden, inter, experts, top_k, local_begin=0, local_count=None,
 
 def opts(gemm_mode=GEMM_AUTO, dense_min_rows=0, pipeline_n=1, gemm_cu_budget=0,
          timing=False, chunk_mode=CHUNK_EXPERTS, exact_order=False, serial=False,
-         dense_tile_rows=0, side_cus=0) -> Opts:
+         dense_tile_rows=0, side_cus=0, group_tile_rows=0) -> Opts:
     """timing: False, True (every phase) or "gemm" (the GEMM launches only).
     exact_order: no K split of the grouped GEMM's last round (the same bits
     for every pipeline number, stage kind, CU budget and GEMM kind).
@@ -143,6 +144,7 @@ def opts(gemm_mode=GEMM_AUTO, dense_min_rows=0, pipeline_n=1, gemm_cu_budget=0,
     o.chunk_mode = chunk_mode
     o.dense_tile_rows = dense_tile_rows
     o.side_cus = side_cus
+    o.group_tile_rows = group_tile_rows
     return o
 
 

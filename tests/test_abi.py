@@ -83,6 +83,8 @@ def test_invalid_options_and_buffers_rejected():
     fake = ctypes.c_void_p(16)
     for o in (moe.opts(pipeline_n=3), moe.opts(pipeline_n=-1), moe.opts(gemm_mode=7),
               moe.opts(gemm_cu_budget=-1), moe.opts(side_cus=-1),
+              moe.opts(group_tile_rows=64), moe.opts(group_tile_rows=-128),
+              moe.opts(dense_tile_rows=100),
               moe.opts(pipeline_n=0, chunk_mode=moe.CHUNK_TOKENS)):
         st = L.moe_ffn_forward(ctypes.byref(d), ctypes.byref(o), fake, fake, None, fake, fake,
                                fake, None, None, None, fake, None, None, None, fake, 1 << 40,
@@ -274,15 +276,33 @@ def test_gemm_plan_model():
     assert tiles[0] in (128, 192, 256, 320)
     assert dense == (dus < gus)
     # forced kinds
-    assert plan(d, moe.opts(gemm_mode=moe.GEMM_GROUP), [4096])[:2] == (False, [320])
-    # a grouped launch's tile height: the smallest that holds its largest
-    # expert below 320 rows (decode batches), else 320
+    assert plan(d, moe.opts(gemm_mode=moe.GEMM_GROUP), [4096])[0] is False
+    # a grouped launch's tile height: never taller than the smallest that
+    # holds its largest expert (320 above 256 rows); among those, the one
+    # the model prices lowest when that is at least 5% below the holding
+    # height's price.  One expert: the dense pick is the model's cheapest
+    # height, so the grouped price lies within 5% above it
     grouped = moe.opts(gemm_mode=moe.GEMM_GROUP)
     assert plan(d, grouped, [1, 0])[1] == [128, 128]
     assert plan(d, grouped, [128, 3])[1] == [128, 128]
-    assert plan(d, grouped, [129])[1] == [192]
-    assert plan(d, grouped, [200, 7])[1] == [256, 256]
-    assert plan(d, grouped, [100, 257])[1] == [320, 320]
+    for rows, hold in (([129], 192), ([200, 7], 256), ([100, 257], 320), ([40] * 20, 128),
+                       ([300] * 20, 320), ([4096], 320), ([8192], 320), ([3200], 320)):
+        for exact in (False, True):
+            o = moe.opts(gemm_mode=moe.GEMM_GROUP, exact_order=exact)
+            _, tiles, gus, dus = plan(d, o, rows)
+            assert len(set(tiles)) == 1 and tiles[0] in (128, 192, 256, 320)
+            assert tiles[0] <= hold
+            if len(rows) == 1:
+                assert dus <= gus * (1 + 1e-9) and gus <= dus / 0.95 * (1 + 1e-9)
+    # a few rows per expert: the 128-row tile (every height holds them in
+    # one tile, and it streams the weights fastest); 300 rows each: one
+    # 320-row tile per expert against three of 128
+    assert plan(d, grouped, [100, 257])[1] == [128, 128]
+    assert plan(d, grouped, [300] * 20)[1] == [320] * 20
+    # a forced grouped height
+    for bm in (128, 192, 256, 320):
+        o = moe.opts(gemm_mode=moe.GEMM_GROUP, group_tile_rows=bm)
+        assert plan(d, o, [40, 0, 700])[1] == [bm] * 3
     dense, tiles, _, _ = plan(d, moe.opts(gemm_mode=moe.GEMM_DENSE), [4096, 0, 17])
     assert dense and tiles[1] == 0 and tiles[0] > 0 and tiles[2] > 0
     dense, tiles, _, _ = plan(d, moe.opts(gemm_mode=moe.GEMM_DENSE, dense_tile_rows=192),
@@ -371,9 +391,10 @@ def test_binding_structs_match_the_header():
     """The ctypes mirrors of moe_opts, moe_timing and moe_pipeline_eval have
     the header's sizes and field order (a mismatch would shift every field
     after it), and convert to dicts."""
-    assert ctypes.sizeof(moe.Opts) == 8 * 4
+    assert ctypes.sizeof(moe.Opts) == 9 * 4
     assert ctypes.sizeof(moe.Timing) == 8 * 4 + 6 * 4
     assert ctypes.sizeof(moe.PipelineEval) == 8 * 8 + 2 * 4
-    assert [f for f, _ in moe.Opts._fields_][-2:] == ["dense_tile_rows", "side_cus"]
+    assert [f for f, _ in moe.Opts._fields_][-3:] == ["dense_tile_rows", "side_cus",
+                                                      "group_tile_rows"]
     assert moe.Timing().as_dict()["pipeline_n"] == 0
     assert set(moe.PipelineEval().as_dict()) >= {"eps0", "eps1", "gain_us", "enabled"}

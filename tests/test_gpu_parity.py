@@ -65,6 +65,10 @@ SPLIT_CASES = {
                     renorm=True),
 }
 CASES.update(SPLIT_CASES)
+# the grouped tile heights the stream-K cases are built for (the library's
+# own choice for experts of a few dozen rows is the 128-row tile, which
+# never takes the stream-K tail)
+SPLIT_TILE_ROWS = {"streamk_gu": 192, "streamk_dn": 256}
 
 _cache = {}
 
@@ -454,9 +458,10 @@ def test_forward_timing_modes(name):
 
 @pytest.mark.parametrize("name", ["tall4", "ragged8", "window"])
 def test_dense_tile_heights(name):
-    """DenseGemm launches with every tile height (128, 192, 256, 320 token
-    rows, forced, and the one the launch-cost model picks): the same bits as
-    GroupGemm in exact order, and within the oracle bar with the K split."""
+    """DenseGemm and GroupGemm launches with every tile height (128, 192,
+    256, 320 token rows, forced, and the one the launch-cost model picks):
+    the same bits as GroupGemm's own choice in exact order, and within the
+    oracle bar with the K split."""
     inp, ids, w = case(name)
     g = Dev(inp)
     s = inp.shape
@@ -469,6 +474,11 @@ def test_dense_tile_heights(name):
             assert torch.equal(y, base), f"dense tile {bm} PN={pn} changes the bits"
         y = g.forward(moe.opts(gemm_mode=moe.GEMM_DENSE, dense_tile_rows=bm)).y
         assert_close(y.cpu().numpy(), ref, f"{name} dense tile {bm} with K split")
+        y = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP, group_tile_rows=bm,
+                               exact_order=True)).y
+        assert torch.equal(y, base), f"group tile {bm} changes the bits"
+        y = g.forward(moe.opts(gemm_mode=moe.GEMM_GROUP, group_tile_rows=bm)).y
+        assert_close(y.cpu().numpy(), ref, f"{name} group tile {bm} with K split")
     # AUTO with one expert per stage may take either kind: same bits again
     y = g.forward(moe.opts(pipeline_n=s.EL, exact_order=True)).y
     assert torch.equal(y, base)
@@ -505,11 +515,13 @@ def test_forward_k_split(name):
     g = Dev(inp)
     s = inp.shape
     ref = oracle_y(inp, ids, w, np.arange(s.T))
-    y = g.forward(moe.opts()).y.clone()
+    bm = SPLIT_TILE_ROWS.get(name, 0)
+    y = g.forward(moe.opts(group_tile_rows=bm)).y.clone()
     assert_close(y.cpu().numpy(), ref, f"{name} split")
     for _ in range(2):
-        assert torch.equal(g.forward(moe.opts()).y, y), "split result not deterministic"
-    ye = g.forward(moe.opts(exact_order=True)).y.clone()
+        assert torch.equal(g.forward(moe.opts(group_tile_rows=bm)).y, y), \
+            "split result not deterministic"
+    ye = g.forward(moe.opts(exact_order=True, group_tile_rows=bm)).y.clone()
     assert_close(ye.cpu().numpy(), ref, f"{name} exact order")
     # where the fp32 down GEMM is cut, the pieces' sums differ from one pass
     # in the last bits somewhere (the evidence that the split ran; a cut
@@ -518,7 +530,8 @@ def test_forward_k_split(name):
         assert not torch.equal(y, ye), "no tile was split"
     assert_close(y.cpu().numpy(), ye.cpu().numpy().astype(np.float64), f"{name} split vs exact",
                  max_abs=2e-3, rel_fro=1e-4)
-    for o in (moe.opts(pipeline_n=2), moe.opts(gemm_cu_budget=48), moe.opts(gemm_cu_budget=96)):
+    for o in (moe.opts(pipeline_n=2, group_tile_rows=bm), moe.opts(gemm_cu_budget=48),
+              moe.opts(gemm_cu_budget=96, group_tile_rows=bm)):
         yo = g.forward(o).y
         assert_close(yo.cpu().numpy(), ref, f"{name} PN={o.pipeline_n} budget={o.gemm_cu_budget}")
 
@@ -569,8 +582,9 @@ def test_k_split_exact_sums(name):
     g = Dev(inp)
     ye = g.forward(moe.opts(exact_order=True)).y.clone()
     assert torch.isfinite(ye).all()
-    for o in (moe.opts(), moe.opts(pipeline_n=2), moe.opts(gemm_cu_budget=48),
-              moe.opts(gemm_cu_budget=96)):
+    bm = SPLIT_TILE_ROWS.get(name, 0)
+    for o in (moe.opts(group_tile_rows=bm), moe.opts(), moe.opts(pipeline_n=2, group_tile_rows=bm),
+              moe.opts(gemm_cu_budget=48, group_tile_rows=bm), moe.opts(gemm_cu_budget=96)):
         y = g.forward(o).y
         assert torch.equal(y, ye), f"{name} PN={o.pipeline_n} budget={o.gemm_cu_budget}"
 

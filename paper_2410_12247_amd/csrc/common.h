@@ -116,6 +116,10 @@ constexpr size_t kNoAllocScratchBytes = size_t(256) << 20;
 // logits: [T][E] fp32 scratch (may be NULL) for the many-expert, few-token
 // path (E > 16, T <= kRouteLogitsMaxTokens).
 constexpr int64_t kRouteLogitsMaxTokens = 4096;
+// Up to this many waves (one per token and block of up to 16 experts) the
+// router runs one chain per lane (few tokens: the chains' latency bounds
+// the router); beyond, the lane-per-token kernels.
+constexpr int64_t kRouteChainMaxWaves = 512;
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                         int32_t *ids, float *w, float *logits, hipStream_t s);
 // Dispatch indices.  tokens_per_stage == 0: buckets are the local experts;

@@ -717,6 +717,217 @@ hipError_t launch_lane_z(const moe_dims &d, const bf16_t *x, const float *wr, co
     return hipGetLastError();
 }
 
+// Few-token router: one wave per token and block of 4 NQ experts; lane l
+// runs the chain of expert e0 + l.  A chain is H dependent fmas whatever
+// the mapping, so at a few tokens (a SIMD for every wave) the chain's
+// latency is the router's time: a dependent fp32 fma issues every ~6
+// cycles when both operands are in vector registers (measured; ~9 when one
+// is a scalar just computed, ~20 per h in the lane-per-token kernel, whose
+// lanes also widen x and meet a barrier every 64 h).  So the wave first
+// widens its token's x row into LDS as fp32 (read back by broadcast: every
+// lane the same address), the router rows stream through an LDS ring by
+// LDS-DMA up to NS - 2 blocks of 64 h ahead (at decode sizes they come from
+// HBM: the expert GEMMs between two forwards evict them), and each half
+// block's operands are read into registers during the previous half's
+// fmas.  The ring is unrolled by slot, so every read has its slot in the
+// instruction's offset.  Same chains (one fp32 fma per h from +0, bias
+// added at the end) and the same selection code as the other kernels, so
+// the same bits.
+namespace chain {
+
+// dynamic LDS of the ring (NS * NQ KB) and the fp32 x row, at most 64 KB
+constexpr size_t kMaxLds = 65536;
+
+struct Half {  // 32 h: x (the same in every lane) and the lane's router row
+    floatx4 x[8], w[8];
+};
+
+// Ring slot layout: row r (lane r's expert) at 256 r, its 16-byte chunk c
+// at position c ^ (r % 16), so the 16 rows one read instruction touches
+// for a given chunk fall on distinct banks.
+template <int OFF>
+__device__ __forceinline__ void read(Half &hv, const char *lds, const int (&woff)[16], int half,
+                                     int xoff) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        hv.w[j] = *reinterpret_cast<const floatx4 *>(lds + OFF + woff[8 * half + j]);
+        hv.x[j] = *reinterpret_cast<const floatx4 *>(lds + xoff + 16 * j);
+    }
+}
+
+__device__ __forceinline__ float run(const Half &hv, float acc) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc = __builtin_fmaf(hv.x[j][c], hv.w[j][c], acc);
+    return acc;
+}
+
+}  // namespace chain
+
+// NQ: router-row DMA requests per block (4 rows of 256 bytes each); NS ring
+// slots, NS - 2 blocks of requests in flight.  ZOUT: logits (bias added) to
+// zout [T][E] for route_select_kernel; else every expert is in the wave
+// (E <= 4 NQ) and it selects in place.  Dynamic LDS: NS * NQ KB of ring,
+// then the fp32 x row.
+// (the body is a device function: the host pass of a kernel template whose
+// own body calls generic lambdas over target builtins emits no launch stub)
+template <int NQ, int NS, bool ZOUT>
+__device__ __forceinline__ void route_chain(char *lds, const bf16_t *__restrict__ x,
+                                            const float *__restrict__ wr,
+                                            const float *__restrict__ bias, int64_t T, int H,
+                                            int E, int k, int renorm,
+                                            int32_t *__restrict__ ids, float *__restrict__ wout,
+                                            float *__restrict__ zout) {
+    constexpr int SLOT = NQ * 1024;  // bytes: 4 NQ rows of 64 fp32
+    constexpr int RING = NS * SLOT;
+    static_assert(NS >= 3 && (NS - 2) * NQ <= 63 && RING <= 65536, "ring");
+    const int64_t t = blockIdx.x;
+    const int lane = threadIdx.x;
+    const int e0 = (int)blockIdx.y * 4 * NQ;
+    const int e = e0 + lane;
+    const bool live = lane < 4 * NQ && e < E;
+    const int nb = H / 64;
+
+    // DMA: request q of a block moves rows 4q .. 4q + 3 (lane l: row 4q +
+    // l / 16 at position l % 16, i.e. chunk (l % 16) ^ (row % 16)); rows
+    // past E repeat the last expert's.  Block b is the scalar offset.
+    const __amdgpu_buffer_rsrc_t wres =
+        __builtin_amdgcn_make_buffer_rsrc((void *)wr, 0, -1, 0x00020000);
+    uint32_t voff[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const int r = 4 * q + lane / 16;
+        const int c = (lane & 15) ^ (r & 15);
+        voff[q] = (uint32_t)(((int64_t)min(e0 + r, E - 1) * H + 4 * c) * 4);
+    }
+    auto issue = [&](int blk, auto slot) {  // block blk (clamped) into a slot
+        constexpr int S = decltype(slot)::value;
+        const int sb = min(blk, nb - 1) * 256;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                wres, (lds_void_t *)(lds + S * SLOT + q * 1024), 16, voff[q], sb, 0, 0);
+    };
+    // x row -> LDS fp32, 8 bf16 per lane per step; the first 4096 h are
+    // requested before the ring's first blocks, so both latencies overlap
+    const bf16_t *xr = x + t * H;
+    auto widen = [&](int i, const u32x4 &v) {
+        const floatx4 lo = {bf16_lo(v[0]), bf16_hi(v[0]), bf16_lo(v[1]), bf16_hi(v[1])};
+        const floatx4 hi = {bf16_lo(v[2]), bf16_hi(v[2]), bf16_lo(v[3]), bf16_hi(v[3])};
+        *reinterpret_cast<floatx4 *>(lds + RING + 4 * i) = lo;
+        *reinterpret_cast<floatx4 *>(lds + RING + 4 * i + 16) = hi;
+    };
+    u32x4 xv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int i = min(lane * 8 + 512 * j, H - 8);  // clamped: rewrites the last 8
+        xv[j] = *reinterpret_cast<const u32x4 *>(xr + i);
+    }
+    lane_unroll<0, NS - 1>([&](auto s) { issue(decltype(s)::value, s); });
+#pragma unroll
+    for (int j = 0; j < 8; ++j) widen(min(lane * 8 + 512 * j, H - 8), xv[j]);
+    for (int i = lane * 8 + 4096; i < H; i += 512)
+        widen(i, *reinterpret_cast<const u32x4 *>(xr + i));
+
+    // this lane's chunk offsets in a slot (idle lanes read row 4 NQ - 1)
+    int woff[16];
+    {
+        const int r = min(lane, 4 * NQ - 1);
+#pragma unroll
+        for (int c = 0; c < 16; ++c) woff[c] = r * 256 + 16 * (c ^ (r & 15));
+    }
+    chain::Half h0, h1;
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 2) * NQ) : "memory");  // block 0 landed
+    chain::read<0>(h0, lds, woff, 0, RING);
+
+    float acc = 0.0f;
+    int blk = 0;
+    // block blk in slot S: its second half is read during the first half's
+    // fmas; then block blk + 1 has landed, block blk + NS - 1 is requested
+    // into the slot block blk - 1 left, and the first half of block blk + 1
+    // is read during the second half's fmas
+    auto body = [&](auto slot) {
+        constexpr int S = decltype(slot)::value;
+        if (blk >= nb) return;
+        const int xb = RING + blk * 256;
+        chain::read<S * SLOT>(h1, lds, woff, 1, xb + 128);
+        __builtin_amdgcn_sched_barrier(0);  // the reads go out before the fmas
+        acc = chain::run(h0, acc);
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 3) * NQ) : "memory");
+        issue(blk + NS - 1, std::integral_constant<int, (S + NS - 1) % NS>{});
+        chain::read<((S + 1) % NS) * SLOT>(h0, lds, woff, 0, RING + min(blk + 1, nb - 1) * 256);
+        __builtin_amdgcn_sched_barrier(0);
+        acc = chain::run(h1, acc);
+        __builtin_amdgcn_sched_barrier(0);
+        ++blk;
+    };
+    while (blk < nb) lane_unroll<0, NS>(body);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the clamped tail requests
+
+    const float z = bias && live ? acc + bias[e] : acc;
+    if constexpr (ZOUT) {
+        if (live) zout[t * E + e] = z;
+        return;
+    }
+    float *zs = reinterpret_cast<float *>(lds);
+    __syncthreads();  // every ring read done before the logits reuse it
+    zs[lane] = z;
+    __syncthreads();
+    if (E <= 16) {
+        if (lane == 0) select_lane<16>(zs, t, E, k, renorm, ids, wout);
+    } else {
+        select_token(zs, t, E, k, renorm, lane, ids, wout);
+    }
+}
+
+template <int NQ, int NS, bool ZOUT>
+__global__ __launch_bounds__(64) void route_chain_kernel(const bf16_t *__restrict__ x,
+                                                         const float *__restrict__ wr,
+                                                         const float *__restrict__ bias,
+                                                         int64_t T, int H, int E, int k,
+                                                         int renorm, int32_t *__restrict__ ids,
+                                                         float *__restrict__ wout,
+                                                         float *__restrict__ zout) {
+    extern __shared__ __attribute__((aligned(16))) char lds[];
+    route_chain<NQ, NS, ZOUT>(lds, x, wr, bias, T, H, E, k, renorm, ids, wout, zout);
+}
+
+template <int NQ, int NS>
+hipError_t launch_chain_q(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
+                          int32_t *ids, float *w, float *z, hipStream_t s) {
+    const dim3 grid((unsigned)d.tokens, (unsigned)((d.experts + 4 * NQ - 1) / (4 * NQ)));
+    const size_t lds = (size_t)NS * NQ * 1024 + (size_t)d.hidden * 4;
+    if (d.experts <= 4 * NQ) {
+        route_chain_kernel<NQ, NS, false><<<grid, 64, lds, s>>>(
+            x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w, nullptr);
+        return hipGetLastError();
+    }
+    route_chain_kernel<NQ, NS, true><<<grid, 64, lds, s>>>(
+        x, wr, bias, d.tokens, d.hidden, d.experts, d.top_k, d.renormalize, ids, w, z);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    route_select_kernel<<<(unsigned)((d.tokens + 3) / 4), RT_THREADS, 0, s>>>(
+        z, d.tokens, d.experts, d.top_k, d.renormalize, ids, w);
+    return hipGetLastError();
+}
+
+// up to 8 experts: one wave of 8 chains; up to 16: one of 16; more: blocks
+// of 16 experts (a wave each) and the selection kernel
+constexpr int kChainSlots = 8;
+int chain_requests(const moe_dims &d) { return d.experts <= 8 ? 2 : 4; }
+bool chain_fits(const moe_dims &d) {
+    return (size_t)kChainSlots * chain_requests(d) * 1024 + (size_t)d.hidden * 4 <=
+           chain::kMaxLds;
+}
+hipError_t launch_chain(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
+                        int32_t *ids, float *w, float *z, hipStream_t s) {
+    if (chain_requests(d) == 2)
+        return launch_chain_q<2, kChainSlots>(d, x, wr, bias, ids, w, z, s);
+    return launch_chain_q<4, kChainSlots>(d, x, wr, bias, ids, w, z, s);
+}
+
 // Per-SIMD fma work of a lane-router shape: every wave issues (G + 1) VALU
 // instructions per h (G fmas and one widening); waves beyond one per SIMD
 // queue behind each other.
@@ -745,6 +956,15 @@ hipError_t launch_lane_router(const moe_dims &d, const bf16_t *x, const float *w
 hipError_t launch_route(const moe_dims &d, const bf16_t *x, const float *wr, const float *bias,
                         int32_t *ids, float *w, float *logits, hipStream_t s) {
     if (d.tokens <= 0) return hipSuccess;
+    // few tokens: the chain-per-lane kernel (its 16-byte loads of x need
+    // the rows 16-byte aligned; more than 16 experts need the logits buffer;
+    // measured against the lane kernels, Mixtral and DBRX shapes: faster up
+    // to 256 tokens, even at 1024, slower at 4096)
+    const int64_t chain_waves =
+        d.tokens * ((d.experts + 4 * chain_requests(d) - 1) / (4 * chain_requests(d)));
+    if (chain_waves <= kRouteChainMaxWaves && chain_fits(d) && ((uintptr_t)x & 15) == 0 &&
+        (d.experts <= 16 || logits))
+        return launch_chain(d, x, wr, bias, ids, w, logits, s);
     if (d.experts <= 16) return launch_lane_router(d, x, wr, bias, ids, w, s);
     // many experts, up to kRouteLogitsMaxTokens tokens: the register-tiled
     // kernel has too few workgroups to cover its serial h loop (or, up to

@@ -178,6 +178,36 @@ def test_route_lane_shapes(T, E, H, k, renorm, use_bias):
     assert weights_match(gw.cpu().numpy(), w)
 
 
+@pytest.mark.parametrize("T,E,H,k,renorm,use_bias", [
+    (1, 8, 4096, 2, True, False),       # decode, Mixtral's router
+    (1, 1, 64, 1, True, True),          # one expert, one block
+    (33, 16, 6144, 4, True, True),      # DBRX's width, 16 lanes
+    (511, 5, 192, 2, False, True),      # three blocks (odd: the pair loop's tail)
+    (512, 8, 64, 2, True, False),       # the last batch size on the chain kernel
+    (513, 8, 64, 2, True, False),       # the first on the lane kernel
+    (32, 16, 8192, 3, False, False),    # the widest 16-expert row in 64 KB of LDS
+    (2, 8, 12288, 2, True, True),       # the widest 8-expert row
+])
+def test_route_chain_shapes(T, E, H, k, renorm, use_bias):
+    """The chain-per-lane router for few tokens (one wave per token, a lane
+    per expert, x widened into LDS, router rows through an LDS ring): 1 to
+    192 blocks of 64 h, odd block counts, the batch-size boundary with the
+    lane kernel, the widest rows that fit, with the bias, against the
+    oracle bit for bit."""
+    rng = np.random.default_rng(2000 + E + T + H)
+    xb = synth.bf16_bits(rng.standard_normal((T, H), dtype=np.float32))
+    wr = rng.standard_normal((E, H), dtype=np.float32) * np.float32(0.02)
+    bias = (rng.standard_normal(E, dtype=np.float32) * np.float32(0.1)) if use_bias else None
+    _, ids, w = oracle.route(xb, wr, bias, k, renorm)
+    d = moe.dims(T, H, 64, E, k, renormalize=renorm)
+    gids = torch.empty((T, k), dtype=torch.int32, device=dev())
+    gw = torch.empty((T, k), dtype=torch.float32, device=dev())
+    moe.route(d, bf16(xb), f32(wr), f32(bias) if use_bias else None, gids, gw)
+    torch.cuda.synchronize()
+    assert np.array_equal(gids.cpu().numpy(), ids)
+    assert weights_match(gw.cpu().numpy(), w)
+
+
 @pytest.mark.parametrize("name,kw", [
     ("tiny", {}),
     ("fine", {}),                                          # shared experts, no renorm
@@ -589,16 +619,18 @@ def test_k_split_exact_sums(name):
         assert torch.equal(y, ye), f"{name} PN={o.pipeline_n} budget={o.gemm_cu_budget}"
 
 
-@pytest.mark.parametrize("T,E,bias", [(1, 17, False), (37, 40, True), (1024, 17, False),
+@pytest.mark.parametrize("T,E,bias", [(1, 17, False), (37, 40, True), (32, 160, True),
+                                       (1024, 17, False),
                                        (1024, 160, True), (1025, 160, False), (64, 32, True),
                                        (33, 256, False), (500, 96, True), (4096, 40, True),
                                        (4097, 40, False)])
 def test_forward_routing_many_experts(T, E, bias):
-    """Routing inside the forward for E > 16: up to 4096 tokens the logits come
-    from the lane-per-token router in blocks of 16 experts (a ragged last
-    block when 16 does not divide E; 33 tokens leave a ragged token block),
-    through the workspace, and a separate selection; above that from the
-    register-tiled router.  Ids, weights, counts and y match the oracle;
+    """Routing inside the forward for E > 16: at a few tokens (tokens x
+    expert blocks of 16 up to 512) from the chain-per-lane router, else up
+    to 4096 tokens from the lane-per-token router, both in blocks of 16
+    experts (a ragged last block when 16 does not divide E; 33 tokens leave
+    a ragged token block), through the workspace, and a separate selection;
+    above that from the register-tiled router.  Ids, weights, counts and y match the oracle;
     duplicated router rows make exact ties, which go to the lower expert
     index."""
     shp = C(name=f"many{T}_{E}", index=214, T=T, H=192, I=64, E=E, EL=4, e0=E - 4, k=6,

@@ -518,6 +518,56 @@ __device__ __forceinline__ void select_lane(const float *zrow, int64_t t, int E,
     }
 }
 
+// select_lane's result for one token of E <= 16 logits (zrow, in LDS), by
+// the whole wave: lane e holds expert e's key, so each of the k rounds is a
+// wave-wide max (the same winners in the same order), and each lane takes
+// one exponential (lane j: selected expert j, or lane e: expert e); the
+// denominator adds the terms one by one in select_lane's order.  The same
+// bits, in the time of two exponentials instead of 2k.
+__device__ __forceinline__ void select_wave16(const float *zrow, int64_t t, int E, int k,
+                                              int renorm, int lane, int32_t *__restrict__ ids,
+                                              float *__restrict__ wout) {
+    const float z = lane < E ? zrow[lane] : 0.0f;
+    uint64_t key = lane < E ? logit_key(z, lane) : 0ull;
+    int sel_e[kMaxTopK];
+    float sel_z[kMaxTopK];
+    int my_e = 0;
+    float my_z = 0.0f;  // lane j < k: the j-th selected expert and logit
+#pragma unroll
+    for (int j = 0; j < kMaxTopK; ++j) {
+        sel_e[j] = 0;
+        sel_z[j] = 0.0f;
+        if (j < k) {
+            const uint64_t best = wave_max_u64(key);
+            sel_e[j] = (int)(0xFFFFFFFFu - (uint32_t)best);
+            sel_z[j] = key_logit(best);
+            if (key == best) key = 0ull;
+            if (lane == j) {
+                my_e = sel_e[j];
+                my_z = sel_z[j];
+            }
+        }
+    }
+    const double zmax = (double)sel_z[0];
+    const double ex_sel = exp((double)my_z - zmax);
+    double denom = 0.0;
+    if (renorm) {
+        const uint64_t b = __builtin_bit_cast(uint64_t, ex_sel);
+#pragma unroll
+        for (int j = 0; j < kMaxTopK; ++j)
+            if (j < k) denom += __builtin_bit_cast(double, readlane64(b, j));
+    } else {
+        const uint64_t b = __builtin_bit_cast(uint64_t, exp((double)z - zmax));
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+            if (e < E) denom += __builtin_bit_cast(double, readlane64(b, e));
+    }
+    if (lane < k) {
+        ids[t * k + lane] = my_e;
+        wout[t * k + lane] = (float)(ex_sel / denom);
+    }
+}
+
 // ZOUT: the workgroup takes experts blockIdx.y * EP .. (any E) and writes
 // its logits (bias added) to zout [T][E] for a selection kernel; else one
 // workgroup holds every expert (E <= EP) and selects in place.
@@ -876,7 +926,7 @@ __device__ __forceinline__ void route_chain(char *lds, const bf16_t *__restrict_
     zs[lane] = z;
     __syncthreads();
     if (E <= 16) {
-        if (lane == 0) select_lane<16>(zs, t, E, k, renorm, ids, wout);
+        select_wave16(zs, t, E, k, renorm, lane, ids, wout);
     } else {
         select_token(zs, t, E, k, renorm, lane, ids, wout);
     }

@@ -813,6 +813,103 @@ __device__ __forceinline__ float run(const Half &hv, float acc) {
     return acc;
 }
 
+// The DPP form: lane n of each 16-lane row holds x[4n .. 4n+3] of the 64-h
+// block (xq; every row reads the same 256 bytes, one read per block instead
+// of sixteen), and the fma for h = 4n + c takes component c broadcast from
+// lane n of its row (row_newbcast).  fma(x, w, acc) is the same operation
+// whichever factor comes first, so the same bits.  Half 0 covers n = 0..7,
+// half 1 n = 8..15; the s_nop covers a DPP source written by the previous
+// vector instruction.
+struct HalfW {  // 32 h of the lane's router row
+    floatx4 w[8];
+};
+template <int OFF>
+__device__ __forceinline__ void read_w(HalfW &hv, const char *lds, const int (&woff)[16],
+                                       int half) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        hv.w[j] = *reinterpret_cast<const floatx4 *>(lds + OFF + woff[8 * half + j]);
+}
+template <int HALF>
+__device__ __forceinline__ float run_dpp(const floatx4 &xq, const HalfW &hv, float acc) {
+    if constexpr (HALF == 0) {
+        asm volatile(
+        "s_nop 1\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w0] row_newbcast:0 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w1] row_newbcast:0 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w2] row_newbcast:0 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w3] row_newbcast:0 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w4] row_newbcast:1 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w5] row_newbcast:1 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w6] row_newbcast:1 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w7] row_newbcast:1 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w8] row_newbcast:2 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w9] row_newbcast:2 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w10] row_newbcast:2 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w11] row_newbcast:2 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w12] row_newbcast:3 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w13] row_newbcast:3 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w14] row_newbcast:3 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w15] row_newbcast:3 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w16] row_newbcast:4 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w17] row_newbcast:4 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w18] row_newbcast:4 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w19] row_newbcast:4 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w20] row_newbcast:5 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w21] row_newbcast:5 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w22] row_newbcast:5 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w23] row_newbcast:5 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w24] row_newbcast:6 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w25] row_newbcast:6 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w26] row_newbcast:6 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w27] row_newbcast:6 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w28] row_newbcast:7 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w29] row_newbcast:7 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w30] row_newbcast:7 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w31] row_newbcast:7 row_mask:0xf bank_mask:0xf\n\t"
+        : [a] "+v"(acc)
+        : [x0] "v"(xq[0]), [x1] "v"(xq[1]), [x2] "v"(xq[2]), [x3] "v"(xq[3]), [w0] "v"(hv.w[0][0]), [w1] "v"(hv.w[0][1]), [w2] "v"(hv.w[0][2]), [w3] "v"(hv.w[0][3]), [w4] "v"(hv.w[1][0]), [w5] "v"(hv.w[1][1]), [w6] "v"(hv.w[1][2]), [w7] "v"(hv.w[1][3]), [w8] "v"(hv.w[2][0]), [w9] "v"(hv.w[2][1]), [w10] "v"(hv.w[2][2]), [w11] "v"(hv.w[2][3]), [w12] "v"(hv.w[3][0]), [w13] "v"(hv.w[3][1]), [w14] "v"(hv.w[3][2]), [w15] "v"(hv.w[3][3]), [w16] "v"(hv.w[4][0]), [w17] "v"(hv.w[4][1]), [w18] "v"(hv.w[4][2]), [w19] "v"(hv.w[4][3]), [w20] "v"(hv.w[5][0]), [w21] "v"(hv.w[5][1]), [w22] "v"(hv.w[5][2]), [w23] "v"(hv.w[5][3]), [w24] "v"(hv.w[6][0]), [w25] "v"(hv.w[6][1]), [w26] "v"(hv.w[6][2]), [w27] "v"(hv.w[6][3]), [w28] "v"(hv.w[7][0]), [w29] "v"(hv.w[7][1]), [w30] "v"(hv.w[7][2]), [w31] "v"(hv.w[7][3]));
+    } else {
+        asm volatile(
+        "s_nop 1\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w0] row_newbcast:8 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w1] row_newbcast:8 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w2] row_newbcast:8 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w3] row_newbcast:8 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w4] row_newbcast:9 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w5] row_newbcast:9 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w6] row_newbcast:9 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w7] row_newbcast:9 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w8] row_newbcast:10 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w9] row_newbcast:10 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w10] row_newbcast:10 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w11] row_newbcast:10 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w12] row_newbcast:11 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w13] row_newbcast:11 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w14] row_newbcast:11 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w15] row_newbcast:11 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w16] row_newbcast:12 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w17] row_newbcast:12 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w18] row_newbcast:12 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w19] row_newbcast:12 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w20] row_newbcast:13 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w21] row_newbcast:13 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w22] row_newbcast:13 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w23] row_newbcast:13 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w24] row_newbcast:14 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w25] row_newbcast:14 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w26] row_newbcast:14 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w27] row_newbcast:14 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x0], %[w28] row_newbcast:15 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x1], %[w29] row_newbcast:15 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x2], %[w30] row_newbcast:15 row_mask:0xf bank_mask:0xf\n\t"
+        "v_fmac_f32_dpp %[a], %[x3], %[w31] row_newbcast:15 row_mask:0xf bank_mask:0xf\n\t"
+        : [a] "+v"(acc)
+        : [x0] "v"(xq[0]), [x1] "v"(xq[1]), [x2] "v"(xq[2]), [x3] "v"(xq[3]), [w0] "v"(hv.w[0][0]), [w1] "v"(hv.w[0][1]), [w2] "v"(hv.w[0][2]), [w3] "v"(hv.w[0][3]), [w4] "v"(hv.w[1][0]), [w5] "v"(hv.w[1][1]), [w6] "v"(hv.w[1][2]), [w7] "v"(hv.w[1][3]), [w8] "v"(hv.w[2][0]), [w9] "v"(hv.w[2][1]), [w10] "v"(hv.w[2][2]), [w11] "v"(hv.w[2][3]), [w12] "v"(hv.w[3][0]), [w13] "v"(hv.w[3][1]), [w14] "v"(hv.w[3][2]), [w15] "v"(hv.w[3][3]), [w16] "v"(hv.w[4][0]), [w17] "v"(hv.w[4][1]), [w18] "v"(hv.w[4][2]), [w19] "v"(hv.w[4][3]), [w20] "v"(hv.w[5][0]), [w21] "v"(hv.w[5][1]), [w22] "v"(hv.w[5][2]), [w23] "v"(hv.w[5][3]), [w24] "v"(hv.w[6][0]), [w25] "v"(hv.w[6][1]), [w26] "v"(hv.w[6][2]), [w27] "v"(hv.w[6][3]), [w28] "v"(hv.w[7][0]), [w29] "v"(hv.w[7][1]), [w30] "v"(hv.w[7][2]), [w31] "v"(hv.w[7][3]));
+    }
+    return acc;
+}
+
 }  // namespace chain
 
 // NQ: router-row DMA requests per block (4 rows of 256 bytes each); NS ring
@@ -887,29 +984,35 @@ __device__ __forceinline__ void route_chain(char *lds, const bf16_t *__restrict_
 #pragma unroll
         for (int c = 0; c < 16; ++c) woff[c] = r * 256 + 16 * (c ^ (r & 15));
     }
-    chain::Half h0, h1;
+    chain::HalfW h0, h1;
+    floatx4 xq[2];  // the x quads of blocks of even and odd index
+    const int xl = RING + 16 * (lane & 15);
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 2) * NQ) : "memory");  // block 0 landed
-    chain::read<0>(h0, lds, woff, 0, RING);
+    chain::read_w<0>(h0, lds, woff, 0);
+    xq[0] = *reinterpret_cast<const floatx4 *>(lds + xl);
 
     float acc = 0.0f;
     int blk = 0;
     // block blk in slot S: its second half is read during the first half's
     // fmas; then block blk + 1 has landed, block blk + NS - 1 is requested
     // into the slot block blk - 1 left, and the first half of block blk + 1
-    // is read during the second half's fmas
+    // (and its x quad) is read during the second half's fmas.  NS is even,
+    // so the slot's parity is the block's.
+    static_assert(NS % 2 == 0, "x quads alternate with the slot's parity");
     auto body = [&](auto slot) {
         constexpr int S = decltype(slot)::value;
         if (blk >= nb) return;
-        const int xb = RING + blk * 256;
-        chain::read<S * SLOT>(h1, lds, woff, 1, xb + 128);
+        chain::read_w<S * SLOT>(h1, lds, woff, 1);
         __builtin_amdgcn_sched_barrier(0);  // the reads go out before the fmas
-        acc = chain::run(h0, acc);
+        acc = chain::run_dpp<0>(xq[S & 1], h0, acc);
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 3) * NQ) : "memory");
         issue(blk + NS - 1, std::integral_constant<int, (S + NS - 1) % NS>{});
-        chain::read<((S + 1) % NS) * SLOT>(h0, lds, woff, 0, RING + min(blk + 1, nb - 1) * 256);
+        chain::read_w<((S + 1) % NS) * SLOT>(h0, lds, woff, 0);
+        xq[(S + 1) & 1] =
+            *reinterpret_cast<const floatx4 *>(lds + xl + min(blk + 1, nb - 1) * 256);
         __builtin_amdgcn_sched_barrier(0);
-        acc = chain::run(h1, acc);
+        acc = chain::run_dpp<1>(xq[S & 1], h1, acc);
         __builtin_amdgcn_sched_barrier(0);
         ++blk;
     };

@@ -180,12 +180,18 @@ __global__ __launch_bounds__(64) void dispatch_one_chunk_kernel(
     __syncthreads();
     const uint64_t lt_mask = (1ull << lane) - 1ull;
     constexpr int NIT = kPermChunk / 64;
+    // groups of 64 slots that hold any (the rest of the unrolled loops is
+    // skipped: decode batches have one or two)
+    const int nit = (int)((nslots + 63) / 64);
     int idv[NIT], bucket[NIT], rank[NIT];
 #pragma unroll
     for (int it = 0; it < NIT; ++it) idv[it] = ids[min<int64_t>(it * 64 + lane, nslots - 1)];
     asm volatile("" ::: "memory");
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
+        bucket[it] = -1;
+        rank[it] = 0;
+        if (it >= nit) continue;
         const int s = it * 64 + lane;
         int e = idv[it] - e0;
         if (s >= nslots || e < 0 || e >= EL) e = -1;
@@ -229,7 +235,7 @@ __global__ __launch_bounds__(64) void dispatch_one_chunk_kernel(
 #pragma unroll
     for (int it = 0; it < NIT; ++it) {
         const int s = it * 64 + lane;
-        if (s < nslots) {
+        if (it < nit && s < nslots) {
             const int e = bucket[it];
             if (e < 0) {
                 slot_row[s] = -1;

@@ -5,12 +5,14 @@
 // another therefore performs exactly the same fma sequence as a single call
 // over all experts and tokens.
 //
-// One wave per token: the wave reads the token's k slot records, orders the
-// selected ones by expert id (each ranked by counting smaller ids), then streams
-// the hidden dimension in 16-byte vectors, four per lane per pass; a pass
+// One wave per token (and, for small batches, per range of the hidden
+// dimension: blockIdx.y): the wave reads the token's k slot records, orders
+// the selected ones by expert id (each ranked by counting smaller ids), then
+// streams its range in 16-byte vectors, four per lane per pass; a pass
 // issues the loads of all of the token's rows before its first fma, so the
 // rows' loads are in flight together (KS, the most rows a token can have
-// here, bounds the registers this takes).
+// here, bounds the registers this takes).  Every output element's sum is
+// the same fma sequence however the range is cut.
 #include "common.h"
 
 namespace moe {
@@ -86,9 +88,13 @@ __global__ __launch_bounds__(256) void combine_kernel(int64_t t_begin, int64_t t
     }
     if (n == 0 && accumulate) return;
     const int vecs = H / 4;  // H is a multiple of 64: vecs is a multiple of 16
+    // this wave's range of vectors: whole passes of 256
+    const int np = (vecs + 255) / 256;
+    const int per = (np + (int)gridDim.y - 1) / (int)gridDim.y * 256;
+    const int v_lo = (int)blockIdx.y * per, v_hi = min(vecs, v_lo + per);
     float4 *yrow = reinterpret_cast<float4 *>(y + t * H);
     // four 16-byte vectors per lane per pass: all loads of a pass in flight
-    for (int v0 = lane; v0 < vecs; v0 += 256) {
+    for (int v0 = v_lo + lane; v0 < v_hi; v0 += 256) {
         float4 acc[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -122,7 +128,7 @@ __global__ __launch_bounds__(256) void combine_kernel(int64_t t_begin, int64_t t
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-            if (v0 + 64 * u < vecs) store_stream(yrow + v0 + 64 * u, acc[u]);
+            if (v0 + 64 * u < v_hi) store_stream(yrow + v0 + 64 * u, acc[u]);
     }
 }
 
@@ -134,12 +140,17 @@ hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, int64_t t
                           hipStream_t s) {
     if (t_end <= t_begin) return hipSuccess;
     const int64_t blocks = (t_end - t_begin + 3) / 4;
+    // few tokens: each token's passes over the hidden dimension spread over
+    // workgroups of their own, so they run side by side instead of one
+    // after another (a pass waits for its rows' loads)
+    const int passes = (d.hidden / 4 + 255) / 256;
+    const int split = blocks * passes <= 2 * (int64_t)device_cu_count() * 4 ? passes : 1;
     // a token has at most k rows in range
     const int ks = d.top_k;
     auto go = [&](auto kernel) {
-        kernel<<<(unsigned)blocks, 256, 0, s>>>(t_begin, t_end, d.hidden, d.top_k, d.local_begin,
-                                                e_first, e_first + e_count, y_perm, ids,
-                                                slot_row, w, y, accumulate);
+        kernel<<<dim3((unsigned)blocks, (unsigned)split), 256, 0, s>>>(
+            t_begin, t_end, d.hidden, d.top_k, d.local_begin, e_first, e_first + e_count, y_perm,
+            ids, slot_row, w, y, accumulate);
         return hipGetLastError();
     };
     if (ks <= 1) return go(combine_kernel<1>);

@@ -103,7 +103,6 @@ WsLayout ws_layout(const moe_dims *d, const moe_opts *opt) {
         L.act = take(sizeof(bf16_t) * L.rcap * d->inter);
         L.y_perm = take(sizeof(float) * L.rcap * d->hidden);
         L.shared_act = take(sizeof(bf16_t) * T * d->shared_inter);
-        L.shared_off = take(sizeof(int32_t) * 2);
         // K-split partials, unless every GEMM is one pass over K
         L.split_part = take((opt->flags & MOE_FLAG_EXACT_ORDER) ? 0 : gemm_split_bytes());
         L.split_meta = take(sizeof(int32_t) * kSplitMetaInts);

@@ -67,7 +67,6 @@ struct WsLayout {
     size_t act;           // bf16  [Rcap][I]
     size_t y_perm;        // fp32  [Rcap][H]
     size_t shared_act;    // bf16  [T][Is]
-    size_t shared_off;    // int32 [2] = {0, T}: the shared FFN as one grouped-GEMM expert
     size_t split_part;    // fp32  K-split partials (gemm_split_bytes; 0 bytes in exact order)
     size_t split_meta;    // int32 [kSplitMetaInts] K-split tail-tile records
     size_t total;
@@ -150,16 +149,19 @@ hipError_t launch_combine(const moe_dims &d, int e_first, int e_count, int64_t t
 // Launches that share the scratch must not overlap.
 // bm: token rows of the tile, any valid_tile_rows value (every height
 // gives the same bits in exact order); group_tile_rows picks it from a
-// bound on the experts' row counts.
+// bound on the experts' row counts.  offsets NULL: a single expert
+// (e_count 1) of rows_one contiguous rows, a count the host knows (the
+// shared FFN over every token).
 hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
                                const int32_t *offsets, const bf16_t *x_rows,
                                const int32_t *row_map, const bf16_t *w_gate,
                                const bf16_t *w_up, bf16_t *act, int grid, float *parts,
-                               int32_t *split_meta, int bm, hipStream_t s);
+                               int32_t *split_meta, int bm, hipStream_t s,
+                               int64_t rows_one = 0);
 hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
                              const int32_t *offsets, const bf16_t *act,
                              const bf16_t *w_down, float *y_perm, int grid, float *parts,
-                             int32_t *split_meta, int bm, hipStream_t s);
+                             int32_t *split_meta, int bm, hipStream_t s, int64_t rows_one = 0);
 // Dense GEMMs over `rows` host-known contiguous rows, one tile per workgroup.
 hipError_t launch_dense_gateup(int64_t rows, int H, int I, const bf16_t *x, const bf16_t *w_gate,
                                const bf16_t *w_up, bf16_t *act, int bm, hipStream_t s);

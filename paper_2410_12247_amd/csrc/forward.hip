@@ -33,12 +33,6 @@
 namespace moe {
 namespace {
 
-// Row offsets {0, T} of the shared FFN run as one grouped-GEMM expert
-// (vector stores from two lanes).
-__global__ void shared_offsets_kernel(int32_t *__restrict__ off, int32_t T) {
-    if (threadIdx.x < 2) off[threadIdx.x] = threadIdx.x == 0 ? 0 : T;
-}
-
 // AUTO weighs GroupGemm against DenseGemm with the launch-cost model only
 // for stages of at most this many experts: every dense launch pays its own
 // partial round of tiles, so with more experts per stage the single grouped
@@ -562,17 +556,14 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         ds.inter = d.shared_inter;
         ds.local_begin = 0;
         ds.local_count = 1;
-        int32_t *soff = reinterpret_cast<int32_t *>(base + L.shared_off);
         MOE_TRY(tm.begin(sm, PH_SHARED));
-        shared_offsets_kernel<<<1, 64, 0, sm>>>(soff, (int32_t)T);
-        MOE_HIP(hipGetLastError());
-        // one expert of T rows, known on the host: the height a dense
-        // launch of those rows takes
+        // one expert of T rows, known on the host (no offsets array): the
+        // height a dense launch of those rows takes
         const int bm_s = dense_tile_rows(T, H, d.shared_inter, grid, split);
-        MOE_HIP(launch_group_gateup(ds, 0, 1, soff, x, nullptr, shared_gate, shared_up,
-                                    shared_act, grid, split_part, split_meta, bm_s, sm));
-        MOE_HIP(launch_group_down(ds, 0, 1, soff, shared_act, shared_down, y, grid, split_part,
-                                  split_meta, bm_s, sm));
+        MOE_HIP(launch_group_gateup(ds, 0, 1, nullptr, x, nullptr, shared_gate, shared_up,
+                                    shared_act, grid, split_part, split_meta, bm_s, sm, T));
+        MOE_HIP(launch_group_down(ds, 0, 1, nullptr, shared_act, shared_down, y, grid,
+                                  split_part, split_meta, bm_s, sm, T));
         MOE_TRY(tm.end(sm));
     }
 

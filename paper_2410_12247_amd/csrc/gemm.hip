@@ -713,7 +713,7 @@ __global__ __launch_bounds__(TP::THREADS) void group_kernel(
     const int32_t *__restrict__ offsets, int e_first, int e_count, const bf16_t *__restrict__ x,
     const int32_t *__restrict__ row_map, int slot_div, const bf16_t *w0s, const bf16_t *w1s,
     int64_t wstride, int N, int K, void *out, int64_t ldo, float *__restrict__ parts,
-    int32_t *__restrict__ split_meta) {
+    int32_t *__restrict__ split_meta, int rows_one) {
     constexpr int BM = TP::BM;
     // one LDS object (stage buffers, then the per-expert offsets and tile
     // prefix sums): the compiler then does not make fragment reads wait for
@@ -724,7 +724,9 @@ __global__ __launch_bounds__(TP::THREADS) void group_kernel(
     const int tid = threadIdx.x;
     const int NT = (N + TP::BNOUT - 1) / TP::BNOUT;
 
-    for (int i = tid; i <= e_count; i += TP::THREADS) s_off[i] = offsets[e_first + i];
+    // offsets NULL: one expert of rows_one rows (known on the host)
+    for (int i = tid; i <= e_count; i += TP::THREADS)
+        s_off[i] = offsets ? offsets[e_first + i] : (i == 0 ? 0 : rows_one);
     __syncthreads();
     // tiles per expert, then an inclusive scan (Hillis-Steele over <= 256)
     int mine = 0;
@@ -1216,11 +1218,12 @@ template <int MODE, class TP>
 hipError_t group_launch(const int32_t *offsets, int e_first, int e_count, const bf16_t *x,
                         const int32_t *row_map, int slot_div, const bf16_t *w0s,
                         const bf16_t *w1s, int64_t wstride, int N, int K, void *out,
-                        int64_t ldo, int grid, float *parts, int32_t *split_meta, hipStream_t s) {
+                        int64_t ldo, int grid, float *parts, int32_t *split_meta, int rows_one,
+                        hipStream_t s) {
     const bool split = parts != nullptr && split_meta != nullptr;
     group_kernel<MODE, TP><<<grid, TP::THREADS, 0, s>>>(
         offsets, e_first, e_count, x, row_map, slot_div, w0s, w1s, wstride, N, K, out, ldo,
-        split ? parts : nullptr, split ? split_meta : nullptr);
+        split ? parts : nullptr, split ? split_meta : nullptr, rows_one);
     if (split) return launch_split_fixup<MODE, TP>(grid, parts, split_meta, out, ldo, s);
     return hipGetLastError();
 }
@@ -1230,11 +1233,11 @@ hipError_t group_launch_bm(int bm, const int32_t *offsets, int e_first, int e_co
                            const bf16_t *x, const int32_t *row_map, int slot_div,
                            const bf16_t *w0s, const bf16_t *w1s, int64_t wstride, int N, int K,
                            void *out, int64_t ldo, int grid, float *parts, int32_t *split_meta,
-                           hipStream_t s) {
+                           int rows_one, hipStream_t s) {
 #define MOE_GROUP_LAUNCH(BMV)                                                                   \
     return group_launch<MODE, TileOf<MODE, BMV>>(offsets, e_first, e_count, x, row_map,       \
                                                  slot_div, w0s, w1s, wstride, N, K, out, ldo, \
-                                                 grid, parts, split_meta, s)
+                                                 grid, parts, split_meta, rows_one, s)
 #if MOE_GEMM_PINGPONG
     switch (bm) {
         case 128: MOE_GROUP_LAUNCH(128);
@@ -1494,21 +1497,25 @@ hipError_t launch_group_gateup(const moe_dims &d, int e_first, int e_count,
                                const int32_t *offsets, const bf16_t *x_rows,
                                const int32_t *row_map, const bf16_t *w_gate,
                                const bf16_t *w_up, bf16_t *act, int grid, float *parts,
-                               int32_t *split_meta, int bm, hipStream_t s) {
+                               int32_t *split_meta, int bm, hipStream_t s, int64_t rows_one) {
     if (e_count <= 0) return hipSuccess;
+    if (!offsets && (e_count != 1 || rows_one < 0 || rows_one > INT32_MAX))
+        return hipErrorInvalidValue;
     return group_launch_bm<0>(bm, offsets, e_first, e_count, x_rows, row_map, d.top_k, w_gate,
                               w_up, (int64_t)d.inter * d.hidden, d.inter, d.hidden, act,
-                              d.inter, grid, parts, split_meta, s);
+                              d.inter, grid, parts, split_meta, (int)rows_one, s);
 }
 
 hipError_t launch_group_down(const moe_dims &d, int e_first, int e_count,
                              const int32_t *offsets, const bf16_t *act,
                              const bf16_t *w_down, float *y_perm, int grid, float *parts,
-                             int32_t *split_meta, int bm, hipStream_t s) {
+                             int32_t *split_meta, int bm, hipStream_t s, int64_t rows_one) {
     if (e_count <= 0) return hipSuccess;
+    if (!offsets && (e_count != 1 || rows_one < 0 || rows_one > INT32_MAX))
+        return hipErrorInvalidValue;
     return group_launch_bm<1>(bm, offsets, e_first, e_count, act, nullptr, 1, w_down, nullptr,
                               (int64_t)d.hidden * d.inter, d.hidden, d.inter, y_perm, d.hidden,
-                              grid, parts, split_meta, s);
+                              grid, parts, split_meta, (int)rows_one, s);
 }
 
 int skinny_down_rows(int64_t max_rows, int64_t active_experts, int N) {

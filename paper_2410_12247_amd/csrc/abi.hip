@@ -64,7 +64,7 @@ bool gather_foldable(const moe_dims &d) {
     return (uint64_t)d.tokens * (uint64_t)d.hidden * 2u < (uint64_t(1) << 32);
 }
 
-WsLayout ws_layout(const moe_dims *d, const moe_opts *opt) {
+WsLayout ws_layout(const moe_dims *d, const moe_opts *opt, bool shared_apart) {
     WsLayout L{};
     const bool forward = opt != nullptr;
     const int nbuckets = forward ? forward_buckets(d, opt) : d->local_count;
@@ -106,6 +106,11 @@ WsLayout ws_layout(const moe_dims *d, const moe_opts *opt) {
         // K-split partials, unless every GEMM is one pass over K
         L.split_part = take((opt->flags & MOE_FLAG_EXACT_ORDER) ? 0 : gemm_split_bytes());
         L.split_meta = take(sizeof(int32_t) * kSplitMetaInts);
+        if (shared_apart && d->shared_inter > 0 && (opt->flags & MOE_FLAG_EXACT_ORDER) == 0 &&
+            (opt->flags & MOE_FLAG_SERIAL) == 0) {
+            L.split_part_sh = take(gemm_split_bytes());
+            L.split_meta_sh = take(sizeof(int32_t) * kSplitMetaInts);
+        }
     }
     L.total = o;
     return L;

@@ -69,6 +69,8 @@ struct WsLayout {
     size_t shared_act;    // bf16  [T][Is]
     size_t split_part;    // fp32  K-split partials (gemm_split_bytes; 0 bytes in exact order)
     size_t split_meta;    // int32 [kSplitMetaInts] K-split tail-tile records
+    size_t split_part_sh; // the shared FFN's own K-split scratch when it may run beside
+    size_t split_meta_sh; //   the routed GEMMs (0: it uses the one above)
     size_t total;
     int64_t nchunks;
     int64_t rcap;
@@ -78,8 +80,10 @@ struct WsLayout {
     int nguards;
 };
 // Layout for moe_permute (o == NULL) or for moe_ffn_forward with options o
-// (valid options: check them first).
-WsLayout ws_layout(const moe_dims *d, const moe_opts *o);
+// (valid options: check them first).  shared_apart: the forward may run the
+// shared FFN beside the routed GEMMs (its own streams), so their K splits
+// need separate scratch; the no-allocation entry point runs one stream.
+WsLayout ws_layout(const moe_dims *d, const moe_opts *o, bool shared_apart = true);
 // The grouped gate/up GEMM can read its token rows straight from x through
 // the dispatch order while every byte offset into x fits 32 bits.
 bool gather_foldable(const moe_dims &d);

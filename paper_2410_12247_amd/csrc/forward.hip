@@ -7,6 +7,8 @@
 //                      dispatch all2all of one stage)
 //   sm (GEMM)        : shared experts, then each stage's expert GEMMs
 //   sc (combine)     : each stage's weighted combine, in stage order
+// With one stage and shared experts only the shared FFN leaves the caller's
+// stream: the routed GEMMs and the combine follow the dispatch on s0.
 // Stage i's GEMMs wait for its gather; its combine waits for its GEMMs, so
 // gather(i+1) and combine(i-1) overlap GEMM(i).  By default a stage is an
 // expert group: local experts [i*EL/PN, (i+1)*EL/PN), whose rows are one
@@ -495,15 +497,17 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         st == nullptr || (PN == 1 && !has_shared) || (o->flags & MOE_FLAG_SERIAL) != 0;
     const int max_pn = PN > 0 ? PN : EL;
     hipEvent_t ev_fork = nullptr, ev_counts = nullptr, ev_done = nullptr, ev_start = nullptr;
+    hipEvent_t ev_shared = nullptr;
     hipEvent_t *ev_g = nullptr, *ev_m = nullptr;
     Streams strm;
     if (st) {
-        MOE_TRY(ensure_events(st->sync_ev, 3 * (size_t)max_pn + 4, hipEventDisableTiming));
+        MOE_TRY(ensure_events(st->sync_ev, 3 * (size_t)max_pn + 5, hipEventDisableTiming));
         ev_fork = st->sync_ev[0];
         ev_counts = st->sync_ev[1];
         ev_done = st->sync_ev[2];
         ev_start = st->sync_ev[3];
-        ev_g = &st->sync_ev[4];
+        ev_shared = st->sync_ev[4];
+        ev_g = &st->sync_ev[5];
         ev_m = ev_g + max_pn;
         if (!one_stream) MOE_TRY(get_streams(st, o->side_cus, &strm));
     }
@@ -546,6 +550,9 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
     const bool split = (o->flags & MOE_FLAG_EXACT_ORDER) == 0;
     float *split_part = split ? reinterpret_cast<float *>(base + L.split_part) : nullptr;
     int32_t *split_meta = split ? reinterpret_cast<int32_t *>(base + L.split_meta) : nullptr;
+    // the shared FFN's K split has scratch of its own when the workspace
+    // holds it (then the routed GEMMs may run beside it)
+    const bool shared_scratch = split && L.split_part_sh != 0;
     if (has_shared) {
         // the shared FFN is one expert of T contiguous rows through the
         // grouped scheduler, whose K split shortens a partial last round of
@@ -560,11 +567,16 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         // one expert of T rows, known on the host (no offsets array): the
         // height a dense launch of those rows takes
         const int bm_s = dense_tile_rows(T, H, d.shared_inter, grid, split);
+        float *sp = shared_scratch ? reinterpret_cast<float *>(base + L.split_part_sh)
+                                   : split_part;
+        int32_t *sq = shared_scratch ? reinterpret_cast<int32_t *>(base + L.split_meta_sh)
+                                     : split_meta;
         MOE_HIP(launch_group_gateup(ds, 0, 1, nullptr, x, nullptr, shared_gate, shared_up,
-                                    shared_act, grid, split_part, split_meta, bm_s, sm, T));
-        MOE_HIP(launch_group_down(ds, 0, 1, nullptr, shared_act, shared_down, y, grid,
-                                  split_part, split_meta, bm_s, sm, T));
+                                    shared_act, grid, sp, sq, bm_s, sm, T));
+        MOE_HIP(launch_group_down(ds, 0, 1, nullptr, shared_act, shared_down, y, grid, sp, sq,
+                                  bm_s, sm, T));
         MOE_TRY(tm.end(sm));
+        if (!one_stream) MOE_HIP(hipEventRecord(ev_shared, sm));
     }
 
     // routing and dispatch indices on the caller stream
@@ -612,9 +624,17 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
     // gets its own stream only when it can run beside a later stage's GEMMs;
     // with one stage it follows them on the GEMM stream.
     const bool combine_apart = !one_stream && PN > 1;
-    hipStream_t scomb = combine_apart ? sc : sm;
+    // One stage beside the shared FFN: the routed GEMMs and the combine
+    // follow the dispatch on the caller's stream (no hop to the GEMM stream
+    // and back); only the combine, which adds onto the shared FFN's output,
+    // waits for it.  This needs the shared FFN's own K-split scratch (the
+    // two may overlap) and the folded gather (no gather stream).
+    const bool routed_on_caller =
+        !one_stream && PN == 1 && has_shared && fold_ok && (!split || shared_scratch);
+    hipStream_t sr = routed_on_caller ? s0 : sm;  // the routed GEMMs' stream
+    hipStream_t scomb = combine_apart ? sc : sr;
 
-    if (!one_stream) {
+    if (!one_stream && !routed_on_caller) {
         MOE_HIP(hipEventRecord(ev_fork, s0));
         if (!fold_ok) MOE_HIP(hipStreamWaitEvent(sg, ev_fork, 0));
         MOE_HIP(hipStreamWaitEvent(sm, ev_fork, 0));
@@ -659,7 +679,7 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
         }
         if (!one_stream && !fold_gather) {
             MOE_HIP(hipEventRecord(ev_g[i], sg));
-            MOE_HIP(hipStreamWaitEvent(sm, ev_g[i], 0));
+            MOE_HIP(hipStreamWaitEvent(sr, ev_g[i], 0));
             tm.gap();
         }
 
@@ -679,14 +699,14 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
                 const int bm = o->dense_tile_rows > 0
                                    ? o->dense_tile_rows
                                    : dense_tile_rows(rows, H, I, grid, split);
-                MOE_TRY(tm.begin(sm, PH_GATEUP));
+                MOE_TRY(tm.begin(sr, PH_GATEUP));
                 MOE_HIP(launch_group_gateup(d, e, 1, goff, xrows, rmap, w_gate, w_up, act, grid,
-                                            split_part, split_meta, bm, sm));
-                MOE_TRY(tm.end(sm));
-                MOE_TRY(tm.begin(sm, PH_DOWN));
+                                            split_part, split_meta, bm, sr));
+                MOE_TRY(tm.end(sr));
+                MOE_TRY(tm.begin(sr, PH_DOWN));
                 MOE_HIP(launch_group_down(d, e, 1, goff, act, w_down, y_perm, grid, split_part,
-                                          split_meta, bm, sm));
-                MOE_TRY(tm.end(sm));
+                                          split_meta, bm, sr));
+                MOE_TRY(tm.end(sr));
                 if (timing) {
                     ++g_timing.gateup_launches;
                     ++g_timing.down_launches;
@@ -703,22 +723,22 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
                         : group_launch_rows(stage_max_rows, need_counts ? &hc[b0] : nullptr,
                                             per_stage, t_hi - t_lo, (double)d.top_k / d.experts,
                                             H, I, grid, split);
-                MOE_TRY(tm.begin(sm, PH_GATEUP));
+                MOE_TRY(tm.begin(sr, PH_GATEUP));
                 MOE_HIP(launch_group_gateup(d, e_w, per_stage, goff, xrows, rmap, w_gate, w_up,
-                                            act, grid, split_part, split_meta, bm, sm));
-                MOE_TRY(tm.end(sm));
+                                            act, grid, split_part, split_meta, bm, sr));
+                MOE_TRY(tm.end(sr));
                 // decode-sized stages with enough tiles: the skinny down tile
                 const int64_t active =
                     std::min<int64_t>(per_stage, (t_hi - t_lo) * (int64_t)d.top_k);
                 const int sk = skinny_down_rows(stage_max_rows, active, H);
-                MOE_TRY(tm.begin(sm, PH_DOWN));
+                MOE_TRY(tm.begin(sr, PH_DOWN));
                 if (sk > 0)
                     MOE_HIP(launch_skinny_down(d, e_w, per_stage, goff, act, w_down, y_perm, sk,
-                                               active, sm));
+                                               active, sr));
                 else
                     MOE_HIP(launch_group_down(d, e_w, per_stage, goff, act, w_down, y_perm, grid,
-                                              split_part, split_meta, bm, sm));
-                MOE_TRY(tm.end(sm));
+                                              split_part, split_meta, bm, sr));
+                MOE_TRY(tm.end(sr));
                 if (timing) {
                     ++g_timing.gateup_launches;
                     ++g_timing.down_launches;
@@ -726,20 +746,24 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
             }
         }
         if (combine_apart) {
-            MOE_HIP(hipEventRecord(ev_m[i], sm));
+            MOE_HIP(hipEventRecord(ev_m[i], sr));
             MOE_HIP(hipStreamWaitEvent(sc, ev_m[i], 0));
             tm.gap();
         }
 
         // weighted combine of this stage: its experts over all tokens, or
-        // all experts over its tokens
+        // all experts over its tokens (after the shared FFN, onto its output)
+        if (routed_on_caller) {
+            MOE_HIP(hipStreamWaitEvent(s0, ev_shared, 0));
+            tm.gap();
+        }
         MOE_TRY(tm.begin(scomb, PH_COMBINE));
         const int accumulate = (has_shared || (!tok_stages && i > 0)) ? 1 : 0;
         MOE_HIP(launch_combine(d, tok_stages ? 0 : b0, tok_stages ? EL : per_stage, t_lo, t_hi,
                                y_perm, ids, slot_row, wts, y, accumulate, scomb));
         MOE_TRY(tm.end(scomb));
     }
-    if (!one_stream) {
+    if (!one_stream && scomb != s0) {
         MOE_HIP(hipEventRecord(ev_done, scomb));
         MOE_HIP(hipStreamWaitEvent(s0, ev_done, 0));
         tm.gap();
@@ -894,7 +918,7 @@ moe_status moe_ffn_forward_noalloc(const moe_dims *dims, const moe_opts *opts,
     if (dims->tokens == 0) return MOE_OK;
     MOE_TRY(check_tensors(*dims, x, w_router, w_gate, w_up, w_down, shared_gate, shared_up,
                           shared_down, y));
-    const WsLayout L = ws_layout(dims, o);
+    const WsLayout L = ws_layout(dims, o, false);
     if (L.total > kNoAllocScratchBytes)
         return fail(MOE_ERR_UNSUPPORTED,
                     "moe_ffn_forward_noalloc: needs %zu bytes of scratch, the built-in "

@@ -671,8 +671,9 @@ def _trace_forwards(path):
     """Kernel dispatches of a kernel-trace CSV in the order they were
     enqueued (dispatch id; kernels on the forward's side streams overlap, and
     a kernel's start stamp can precede that of the one before it on its own
-    stream), cut into forwards: each starts at the shared-expert offsets
-    kernel when the workload has shared experts, else at the router."""
+    stream), cut into forwards: each runs from the first kernel after the
+    previous forward's last combine (the shared FFN's GEMMs, enqueued before
+    the router, when the workload has shared experts) through its own."""
     import csv
 
     ev = []
@@ -681,11 +682,18 @@ def _trace_forwards(path):
                    int(r["End_Timestamp"]), _kernel_label(r.get("Kernel_Name", ""))))
     ev.sort(key=lambda e: (e[0], e[1]))
     ev = [e[1:] for e in ev]
-    has_shared = any("shared_offsets" in e[2] for e in ev)
-    first = (lambda n: "shared_offsets" in n) if has_shared else \
-        (lambda n: n.startswith("route") and "select" not in n)
-    starts = [i for i, e in enumerate(ev) if first(e[2])]
+    routers = [i for i, e in enumerate(ev)
+               if e[2].startswith("route") and "select" not in e[2]]
+    starts = []
+    for r in routers:
+        i = r - 1
+        while i >= 0 and not ev[i][2].startswith("combine"):
+            i -= 1
+        starts.append(i + 1)
     fwd = [ev[a:b] for a, b in zip(starts, starts[1:] + [len(ev)])]
+    # shared experts: grouped GEMM launches ahead of a forward's router
+    has_shared = any(e[2].startswith("group_kernel")
+                     for a, r in zip(starts, routers) for e in ev[a:r])
     return fwd, has_shared
 
 

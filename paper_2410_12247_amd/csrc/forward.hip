@@ -35,6 +35,10 @@
 namespace moe {
 namespace {
 
+// The routed GEMMs run beside the shared FFN (one stage) up to this many
+// tokens.
+constexpr int64_t kRoutedBesideSharedMaxTokens = 4096;
+
 // AUTO weighs GroupGemm against DenseGemm with the launch-cost model only
 // for stages of at most this many experts: every dense launch pays its own
 // partial round of tiles, so with more experts per stage the single grouped
@@ -628,9 +632,14 @@ moe_status forward_impl(const moe_dims &d, const moe_opts &opt, const moe_bf16 *
     // follow the dispatch on the caller's stream (no hop to the GEMM stream
     // and back); only the combine, which adds onto the shared FFN's output,
     // waits for it.  This needs the shared FFN's own K-split scratch (the
-    // two may overlap) and the folded gather (no gather stream).
-    const bool routed_on_caller =
-        !one_stream && PN == 1 && has_shared && fold_ok && (!split || shared_scratch);
+    // two may overlap) and the folded gather (no gather stream).  Up to
+    // kRoutedBesideSharedMaxTokens tokens: beyond, both GEMMs fill the chip
+    // and running them side by side saves nothing (measured on the
+    // DeepSeekV2 shape: -9% at 64 tokens, -4% at 4096, -0.7% at 16384,
+    // where each GEMM then takes twice as long as alone).
+    const bool routed_on_caller = !one_stream && PN == 1 && has_shared && fold_ok &&
+                                  (!split || shared_scratch) &&
+                                  T <= kRoutedBesideSharedMaxTokens;
     hipStream_t sr = routed_on_caller ? s0 : sm;  // the routed GEMMs' stream
     hipStream_t scomb = combine_apart ? sc : sr;
 
